@@ -1,0 +1,125 @@
+"""CPU oracle of the ASD verifier -- TEST INFRASTRUCTURE ONLY.
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library never does, and it
+shares no code with the HIP path.
+
+The arithmetic lives in ``asd_oracle.c`` (plain sequential C); this module only
+marshals numpy arrays to it.  Logits are numpy ``float32`` arrays, or ``uint16``
+arrays holding bf16 bit patterns.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from .build import LIBRARY, build_oracle
+
+F32 = 0
+BF16 = 1
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIBRARY):
+            build_oracle()
+        lib = ctypes.CDLL(LIBRARY)
+        i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+        lib.oracle_ranks_above.argtypes = [f32, f32]
+        lib.oracle_ranks_above.restype = ctypes.c_int
+        lib.oracle_row_argmax.argtypes = [vp, ctypes.c_int, i64, i64]
+        lib.oracle_row_argmax.restype = i64
+        lib.oracle_argmax_rows.argtypes = [vp, ctypes.c_int, i64, i64, vp]
+        lib.oracle_argmax_rows.restype = None
+        lib.oracle_block.argtypes = [i32, vp, vp, vp, vp, vp, f32, vp, f32, i32, vp, vp, vp]
+        lib.oracle_block.restype = None
+        lib.oracle_verify.argtypes = [vp, ctypes.c_int, i64, i32, i64, vp, vp, vp, vp, vp, vp,
+                                      vp, vp, vp, vp]
+        lib.oracle_verify.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dtype_code(logits):
+    if logits.dtype == np.float32:
+        return F32
+    if logits.dtype == np.uint16:
+        return BF16
+    raise TypeError("logits must be float32 or uint16 (bf16 bit patterns), got %s" % logits.dtype)
+
+
+def ranks_above(a, b):
+    """True if logit value ``a`` ranks strictly above ``b`` in the argmax order."""
+    return bool(_load().oracle_ranks_above(float(np.float32(a)), float(np.float32(b))))
+
+
+def argmax_rows(logits):
+    """Eq. 1 on every row of a [R, V] array: lowest index of the greatest value."""
+    logits = np.ascontiguousarray(logits)
+    code = _dtype_code(logits)
+    rows, vocab = logits.shape
+    out = np.empty(rows, dtype=np.int32)
+    _load().oracle_argmax_rows(_ptr(logits), code, vocab, rows, _ptr(out))
+    return out
+
+
+def block(x, x_valid, y, z_y, z_x, B, s, g, M):
+    """Algorithm 1 for one draft block.
+
+    ``x`` (K,), ``x_valid`` (K,), ``y`` (K+1,), ``z_y`` (K,), ``z_x`` (K,).
+    Returns ``(a, next_token, s_new, r)``.
+    """
+    x = np.ascontiguousarray(x, dtype=np.int32)
+    K = x.shape[0]
+    x_valid = np.ascontiguousarray(x_valid, dtype=np.uint8)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    z_y = np.ascontiguousarray(z_y, dtype=np.float32)
+    z_x = np.ascontiguousarray(z_x, dtype=np.float32)
+    assert x_valid.shape == (K,) and y.shape == (K + 1,) and z_y.shape == (K,) and z_x.shape == (K,)
+    s_box = np.array([s], dtype=np.float32)
+    a = np.zeros(1, dtype=np.int32)
+    nxt = np.zeros(1, dtype=np.int32)
+    r = np.zeros(max(K, 1), dtype=np.float32)
+    _load().oracle_block(K, _ptr(x), _ptr(x_valid), _ptr(y), _ptr(z_y), _ptr(z_x),
+                         float(np.float32(B)), _ptr(s_box), float(np.float32(g)), int(M),
+                         _ptr(a), _ptr(nxt), _ptr(r))
+    return int(a[0]), int(nxt[0]), np.float32(s_box[0]), r[:K].copy()
+
+
+def verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets=None):
+    """The whole verifier call on host arrays.
+
+    ``budget`` is a float32 [B, 2] array of (total, spent); a new array with the
+    updated ledger is returned (the input is not modified).
+    Returns a dict with ``accept_len``, ``next_token``, ``budget``, ``argmax``,
+    ``regret`` (regret rows that belong to no verified request hold NaN).
+    """
+    logits = np.ascontiguousarray(logits)
+    code = _dtype_code(logits)
+    rows, vocab = logits.shape
+    draft = np.ascontiguousarray(draft_tokens, dtype=np.int32)
+    lens = np.ascontiguousarray(block_lens, dtype=np.int32)
+    nreq = lens.shape[0]
+    tau = np.ascontiguousarray(np.broadcast_to(np.asarray(tau, dtype=np.float32), (nreq,)))
+    cap = np.ascontiguousarray(np.broadcast_to(np.asarray(exc_cap, dtype=np.int32), (nreq,)))
+    bud = np.array(budget, dtype=np.float32, copy=True).reshape(nreq, 2)
+    offs = None if row_offsets is None else np.ascontiguousarray(row_offsets, dtype=np.int64)
+    assert draft.shape == (rows,)
+    accept = np.zeros(nreq, dtype=np.int32)
+    nxt = np.zeros(nreq, dtype=np.int32)
+    amax = np.zeros(rows, dtype=np.int32)
+    regret = np.full(rows, np.nan, dtype=np.float32)
+    rc = _load().oracle_verify(_ptr(logits), code, vocab, nreq, rows, _ptr(draft), _ptr(lens),
+                               _ptr(offs), _ptr(tau), _ptr(cap), _ptr(bud), _ptr(accept),
+                               _ptr(nxt), _ptr(amax), _ptr(regret))
+    if rc != 0:
+        raise ValueError("oracle_verify rejected its arguments (code %d)" % rc)
+    return {"accept_len": accept, "next_token": nxt, "budget": bud, "argmax": amax,
+            "regret": regret}

@@ -1,0 +1,310 @@
+/*
+ * CPU oracle for the verifier of Approximate Speculative Decoding (ASD).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
+ * includes this file; only the test-suite, the smoke check and the CPU
+ * baseline leg of the benchmark load it.  It shares no code, header or helper
+ * with the HIP path.
+ *
+ * It is a plain, slow, sequential statement of what the verifier computes:
+ *
+ *   1. For every target logit row z_i the greedy token y*_i = argmax_v z_i(v)
+ *      (Sec. 3.1, Eq. 1).  Ties go to the lowest index.
+ *   2. For every draft block, Algorithm 1 (Sec. 3.2) in its own order:
+ *      the B = 0 dispatch to exact greedy verification (Eq. 2); the mismatch
+ *      indicator d_i (Eq. 5) and local regret r_i (Eq. 3); the remaining
+ *      length q_i (Eq. 6); the cumulative regret C_i and count N_i (Eq. 8);
+ *      the feasibility mask f_i (Sec. 3.3, Eq. 14, built from the gate of
+ *      Eq. 7 and the constraints of Eqs. 9-11); the longest all-true prefix
+ *      a (Eq. 12); the ledger update s' = s + C_a (Sec. 3.3, Eq. 13); and the
+ *      recovery token y*_{a+1} or, when a = K, the bonus token y*_{K+1}.
+ *   Equations are numbered in the order the paper numbers them: 1 target rows,
+ *   2 strict prefix, 3 local regret, 4 opportunity, 5 mismatch indicator,
+ *   6 remaining length, 7 normalized gate, 8 cumulative state, 9 budget,
+ *   10 block cap, 11 gate for every mismatch, 12 longest feasible prefix,
+ *   13 ledger update, 14 feasibility mask.
+ *
+ * Readings taken where the paper does not fix a detail (each is listed, with
+ * its reason, in the design notes of the repository):
+ *   - argmax order: numeric order of the values, with -0 and +0 equal; NaNs
+ *     are placed by the IEEE 754-2008 totalOrder predicate (a NaN with the
+ *     sign bit clear ranks above +inf, one with it set below -inf, NaNs of one
+ *     sign ordered by payload).  Lowest index wins among equal values.
+ *   - r_i is one binary32 subtraction of the binary32 values (a bf16 logit is
+ *     widened to binary32 exactly first); C_i is a binary32 running sum from
+ *     +0 in position order; s' is one binary32 addition s + C_a, and s is left
+ *     untouched when no mismatch was accepted.
+ *   - gate (Eqs. 7, 11) r_i / q_i <= g is decided as the real-number inequality
+ *     r_i <= g * q_i, evaluated in binary64 (exact for q_i < 2^29).
+ *   - budget (Eq. 9) C_t <= B - s is decided as fl32(s + C_t) <= B, which
+ *     makes the paper's s' <= B hold exactly after rounding.
+ *   - block cap (Eq. 10) N_t <= M.
+ *   - the B = 0 dispatch tests the total budget B (so -0 counts as zero).
+ *   - a draft id outside [0, V) is a mismatch that is never feasible, with
+ *     r = +inf.
+ *   - the bonus row's draft entry is ignored and its regret output is +0.
+ *   - a request whose rows do not fit in [0, total_rows) or whose K is
+ *     negative is not verified: a = 0, next token = -1, state untouched.
+ *
+ * Parity unpinned: none of the functions below is unpinned; the seeded input
+ * generators live elsewhere and are described with the workloads.
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_F32 0
+#define ORACLE_BF16 1
+
+/* ---------------------------------------------------------------- values */
+
+/* A bf16 value is the upper half of a binary32 value: widening is exact. */
+static float bf16_bits_to_float(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+static float logit_at(const void *logits, int dtype, int64_t vocab,
+                      int64_t row, int64_t col)
+{
+    int64_t k = row * vocab + col;
+    if (dtype == ORACLE_BF16)
+        return bf16_bits_to_float(((const uint16_t *)logits)[k]);
+    return ((const float *)logits)[k];
+}
+
+static uint32_t float_bits(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    return u;
+}
+
+/*
+ * Does value a rank strictly above value b?
+ * Non-NaN values: the ordinary IEEE comparison a > b (so -0 and +0 tie).
+ * NaNs: IEEE 754-2008 section 5.10 totalOrder -- positive NaNs lie above every
+ * number, negative NaNs below every number; two positive NaNs are ordered by
+ * payload (larger above), two negative NaNs by payload reversed.
+ */
+int oracle_ranks_above(float a, float b)
+{
+    int a_nan = isnan(a), b_nan = isnan(b);
+    if (!a_nan && !b_nan)
+        return a > b;
+    if (a_nan && !b_nan)
+        return !signbit(a);
+    if (!a_nan && b_nan)
+        return signbit(b) ? 1 : 0;
+    /* both NaN */
+    if (signbit(a) != signbit(b))
+        return !signbit(a);
+    {
+        uint32_t pa = float_bits(a) & 0x007fffffu;
+        uint32_t pb = float_bits(b) & 0x007fffffu;
+        return signbit(a) ? (pa < pb) : (pa > pb);
+    }
+}
+
+/* Eq. 1: y*_i = argmax_v z_i(v); the first (lowest) index among equals. */
+int64_t oracle_row_argmax(const void *logits, int dtype, int64_t vocab,
+                          int64_t row)
+{
+    int64_t best = 0;
+    for (int64_t v = 1; v < vocab; ++v)
+        if (oracle_ranks_above(logit_at(logits, dtype, vocab, row, v),
+                               logit_at(logits, dtype, vocab, row, best)))
+            best = v;
+    return best;
+}
+
+/* Eq. 1 for rows [0, total_rows): out[row] = y*_row. */
+void oracle_argmax_rows(const void *logits, int dtype, int64_t vocab,
+                        int64_t total_rows, int32_t *out)
+{
+    for (int64_t row = 0; row < total_rows; ++row)
+        out[row] = (int32_t)oracle_row_argmax(logits, dtype, vocab, row);
+}
+
+/* ------------------------------------------------------------ Algorithm 1 */
+
+/*
+ * Algorithm 1 for one draft block of length K >= 0.
+ *
+ * Inputs are the ones the algorithm requires:
+ *   x[0..K-1]        the draft block x_1..x_K (token ids)
+ *   x_valid[0..K-1]  1 if x_i is a vocabulary id (0 <= x_i < V), else 0
+ *   y[0..K]          the target greedy tokens y*_1..y*_{K+1}
+ *   z_y[0..K-1]      the target logits z_i(y*_i)
+ *   z_x[0..K-1]      the target logits z_i(x_i) (not read where x_valid == 0)
+ *   B_total, *s      the request state (B, s); *s is updated in place
+ *   g, M             the local gate and the per-block exception cap
+ * Outputs: *a (accepted prefix length) and *next (recovery or bonus token);
+ * r_out[0..K-1] receives r_i when non-NULL.
+ */
+void oracle_block(int32_t K, const int32_t *x, const uint8_t *x_valid,
+                  const int32_t *y, const float *z_y, const float *z_x,
+                  float B_total, float *s, float g, int32_t M,
+                  int32_t *a_out, int32_t *next_out, float *r_out)
+{
+    int32_t a;
+
+    /* Regret (Eq. 3) is reported for every draft position on both paths. */
+    float *r = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
+    uint8_t *d = (uint8_t *)malloc((size_t)(K > 0 ? K : 1));
+    for (int32_t i = 0; i < K; ++i) {
+        d[i] = (!x_valid[i] || x[i] != y[i]) ? 1 : 0;            /* Eq. 5 */
+        r[i] = x_valid[i] ? (z_y[i] - z_x[i]) : INFINITY;        /* Eq. 3 */
+        if (r_out)
+            r_out[i] = r[i];
+    }
+
+    if (B_total == 0.0f) {
+        /* B = 0: exact greedy verification (Eq. 2), state unchanged. */
+        a = 0;
+        while (a < K && x_valid[a] && x[a] == y[a])
+            ++a;
+    } else {
+        int32_t *q = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K > 0 ? K : 1));
+        float *C = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
+        int64_t *N = (int64_t *)malloc(sizeof(int64_t) * (size_t)(K > 0 ? K : 1));
+        uint8_t *f = (uint8_t *)malloc((size_t)(K > 0 ? K : 1));
+        float C_prev = 0.0f;
+        int64_t N_prev = 0;
+
+        for (int32_t i = 0; i < K; ++i)
+            q[i] = K - (i + 1) + 1;                               /* Eq. 6 */
+
+        for (int32_t i = 0; i < K; ++i) {                         /* Eq. 8 */
+            /* d_i r_i adds nothing at a match (r_i there may be inf/NaN). */
+            C[i] = d[i] ? (C_prev + r[i]) : C_prev;
+            N[i] = N_prev + d[i];
+            C_prev = C[i];
+            N_prev = N[i];
+        }
+
+        for (int32_t i = 0; i < K; ++i) {                         /* Eq. 14 */
+            int gate = (double)r[i] <= (double)g * (double)q[i];  /* Eqs. 7, 11 */
+            int budget = (float)(*s + C[i]) <= B_total;           /* Eq. 9 */
+            int cap = N[i] <= (int64_t)M;                         /* Eq. 10 */
+            f[i] = x_valid[i] && (!d[i] || (gate && budget && cap));
+        }
+
+        a = 0;                   /* Eq. 12: longest all-true prefix of f */
+        while (a < K && f[a])
+            ++a;
+
+        if (a > 0 && N[a - 1] > 0)                                /* Eq. 13 */
+            *s = *s + C[a - 1];
+
+        free(q);
+        free(C);
+        free(N);
+        free(f);
+    }
+
+    *a_out = a;
+    *next_out = y[a];   /* recovery y*_{a+1} if a < K, bonus y*_{K+1} if a = K */
+    free(r);
+    free(d);
+}
+
+/* ------------------------------------------------------- whole verifier call */
+
+/*
+ * The whole verification call over a batch, on host arrays.
+ *
+ * logits        [total_rows, vocab] row-major; binary32 (dtype 0) or bf16 bit
+ *               patterns (dtype 1)
+ * draft         [total_rows]; row o_i + p - 1 holds draft x_p of request i;
+ *               the bonus row's entry is ignored
+ * block_lens    [num_requests] K_i
+ * row_offsets   [num_requests] first row o_i of each request, or NULL for the
+ *               packed layout o_i = sum_{j<i} (max(K_j, 0) + 1)
+ * tau           [num_requests] local gate g of each request
+ * exc_cap       [num_requests] block cap M of each request
+ * budget        [num_requests][2] = (B, s); s updated in place
+ * out_accept_len, out_next_token [num_requests]
+ * out_argmax    [total_rows] or NULL: y* of every row
+ * out_regret    [total_rows] or NULL: r of every draft row of a verified
+ *               request, +0 for its bonus row; other rows are not written
+ * Returns 0, or 1 for an argument the call cannot work with.
+ */
+int oracle_verify(const void *logits, int dtype, int64_t vocab,
+                  int32_t num_requests, int64_t total_rows,
+                  const int32_t *draft, const int32_t *block_lens,
+                  const int64_t *row_offsets, const float *tau,
+                  const int32_t *exc_cap, float *budget,
+                  int32_t *out_accept_len, int32_t *out_next_token,
+                  int32_t *out_argmax, float *out_regret)
+{
+    int32_t *y_all;
+    int64_t packed_offset = 0;
+
+    if (vocab < 1 || num_requests < 0 || total_rows < 0 ||
+        (dtype != ORACLE_F32 && dtype != ORACLE_BF16))
+        return 1;
+
+    y_all = (int32_t *)malloc(sizeof(int32_t) * (size_t)(total_rows > 0 ? total_rows : 1));
+    for (int64_t row = 0; row < total_rows; ++row) {
+        y_all[row] = (int32_t)oracle_row_argmax(logits, dtype, vocab, row);
+        if (out_argmax)
+            out_argmax[row] = y_all[row];
+    }
+
+    for (int32_t i = 0; i < num_requests; ++i) {
+        int32_t K = block_lens[i];
+        int64_t o = row_offsets ? row_offsets[i] : packed_offset;
+        packed_offset += (int64_t)(K > 0 ? K : 0) + 1;
+
+        if (K < 0 || o < 0 || o + (int64_t)K >= total_rows) {
+            out_accept_len[i] = 0;
+            out_next_token[i] = -1;
+            continue;
+        }
+
+        {
+            int32_t *x = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K > 0 ? K : 1));
+            uint8_t *x_valid = (uint8_t *)malloc((size_t)(K > 0 ? K : 1));
+            float *z_y = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
+            float *z_x = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
+            float *r = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
+            const int32_t *y = y_all + o;
+            int32_t a = 0, next = -1;
+            float s = budget[2 * i + 1];
+
+            for (int32_t p = 0; p < K; ++p) {
+                int64_t row = o + p;
+                x[p] = draft[row];
+                x_valid[p] = (x[p] >= 0 && (int64_t)x[p] < vocab) ? 1 : 0;
+                z_y[p] = logit_at(logits, dtype, vocab, row, y[p]);
+                z_x[p] = x_valid[p] ? logit_at(logits, dtype, vocab, row, x[p]) : 0.0f;
+            }
+
+            oracle_block(K, x, x_valid, y, z_y, z_x, budget[2 * i], &s,
+                         tau[i], exc_cap[i], &a, &next, r);
+
+            budget[2 * i + 1] = s;
+            out_accept_len[i] = a;
+            out_next_token[i] = next;
+            if (out_regret) {
+                for (int32_t p = 0; p < K; ++p)
+                    out_regret[o + p] = r[p];
+                out_regret[o + K] = 0.0f;
+            }
+            free(x);
+            free(x_valid);
+            free(z_y);
+            free(z_x);
+            free(r);
+        }
+    }
+
+    free(y_all);
+    return 0;
+}
