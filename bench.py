@@ -1,0 +1,253 @@
+"""Benchmark of the ASD verifier on one MI355X.
+
+A step is one ``asd_verify`` call over one batch of draft blocks whose target
+logits are already resident in HBM: the vocabulary-wide argmax of every row
+fused with the draft-logit gather and regret, then Algorithm 1 on every
+request.  The default workload is the headline shape: 256 requests, K = 16
+(4,352 rows), V = 151,936 bf16 logits (1.32 GB per call).
+
+Prints one JSON line on stdout; progress goes to stderr.
+
+    python bench.py [--steps K] [--warmup W] [--config 2|3|4|5] [--gpus 1]
+    python bench.py --copy-calibration     # plain copy of known size, for
+                                           # scaling rocprofv3 FETCH/WRITE_SIZE
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verified logit rows/s + achieved HBM GB/s (B=256,K=16,V=151936 bf16)"
+PEAK_HBM_GBPS = 8000.0
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_03447_amd", "csrc", f)
+                  for f in ("asd_kernels.hip", "asd_plan.h", "asd_api.cpp")]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(w) -> int:
+    """Bytes one call must move at minimum: every logit once, the draft ids, and
+    per request K, g, M, the ledger (read 8, write 4) and the two outputs."""
+    rows = w.rows_per_call
+    return rows * w.vocab * w.logits.itemsize + 4 * rows + 32 * w.num_requests
+
+
+def read_traffic(workload_tag: str, source_hash: str):
+    """HBM bytes per call from the committed rocprofv3 counter summary, scaled by
+    the copy-kernel calibration; None when absent or taken on other sources."""
+    path = os.path.join(PROFILE_DIR, "asd_row_kernel_%s_pmc.md" % workload_tag)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    vals = {}
+    for key in ("source_sha256_16", "fetch_bytes_per_call_scaled", "write_bytes_per_call_scaled"):
+        m = re.search(r"%s:\s*([0-9a-f.]+)" % key, text)
+        if m:
+            vals[key] = m.group(1)
+    if vals.get("source_sha256_16") != source_hash:
+        return None
+    try:
+        return int(float(vals["fetch_bytes_per_call_scaled"]) +
+                   float(vals["write_bytes_per_call_scaled"]))
+    except KeyError:
+        return None
+
+
+def copy_calibration(torch, nbytes=1 << 30, reps=10):
+    """Plain device copy of a known size (rocprofv3 --pmc calibration run)."""
+    dev = torch.device("cuda:0")
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes,
+                      "reps": reps}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="bound on the CPU-oracle baseline's timed work")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this verifier build runs on a single MI355X and "
+              "has no multi-GPU path (--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
+
+    import paper_2608_03447_amd as asd
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    w = W.make_config(args.config)
+    log("workload %s: %d rows x %d (%s), %.2f GB logits, generated in %.1fs" % (
+        w.name, w.rows_per_call, w.vocab, w.dtype, w.logit_bytes_per_call / 1e9, time.time() - t0))
+
+    if w.dtype == "bf16":
+        logits = torch.from_numpy(w.logits.view(np.int16)).to(dev).view(torch.bfloat16)
+    else:
+        logits = torch.from_numpy(w.logits).to(dev)
+    draft = torch.from_numpy(w.draft_tokens).to(dev)
+    lens = torch.from_numpy(w.block_lens).to(dev)
+    tau = torch.from_numpy(w.tau).to(dev)
+    cap = torch.from_numpy(w.exc_cap).to(dev)
+    pristine = torch.from_numpy(w.budget.copy()).to(dev)
+    budget = pristine.clone()
+    acc = torch.empty(w.num_requests, dtype=torch.int32, device=dev)
+    nxt = torch.empty(w.num_requests, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        asd.asd_verify(logits, draft, lens, tau, cap, budget, out_accept_len=acc,
+                       out_next_token=nxt)
+
+    # Parity call on the pristine ledger (checked against the oracle below).
+    step()
+    torch.cuda.synchronize()
+    gpu_out = (acc.cpu().numpy().copy(), nxt.cpu().numpy().copy(),
+               budget.cpu().numpy().copy())
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream(dev)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t_begin = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_begin.record(stream)
+    for k in range(args.steps):
+        starts[k].record(stream)
+        step()
+        ends[k].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_begin.elapsed_time(t_end)
+    per_call_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    avg_call_ms = sum(per_call_ms) / len(per_call_ms)
+    ms_per_step = total_ms / args.steps
+    rows_per_s = w.rows_per_call * args.steps / (total_ms / 1e3)
+    alg_bytes = algorithmic_bytes(w)
+    achieved = alg_bytes / (avg_call_ms / 1e3) / 1e9
+    log("timed %d calls: %.2f ms total (%.3f ms/call, median %.3f, min %.3f), wall %.3fs" % (
+        args.steps, total_ms, ms_per_step, statistics.median(per_call_ms), min(per_call_ms), wall))
+
+    # Practical read roofline on this machine: torch's reduction over the same logits.
+    probe = logits.view(torch.int16) if w.dtype == "bf16" else logits
+    for _ in range(3):
+        probe.sum(dtype=torch.int64 if w.dtype == "bf16" else torch.float32)
+    pe0 = torch.cuda.Event(enable_timing=True)
+    pe1 = torch.cuda.Event(enable_timing=True)
+    pe0.record(stream)
+    for _ in range(10):
+        probe.sum(dtype=torch.int64 if w.dtype == "bf16" else torch.float32)
+    pe1.record(stream)
+    torch.cuda.synchronize()
+    probe_gbps = w.logit_bytes_per_call * 10 / (pe0.elapsed_time(pe1) / 1e3) / 1e9
+
+    # Oracle: parity reference and CPU baseline (single-threaded, as written).
+    parity = "not checked"
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        times = []
+        ref = None
+        while True:
+            c0 = time.perf_counter()
+            ref = oracle.verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap,
+                                w.budget)
+            times.append(time.perf_counter() - c0)
+            if sum(times) >= args.cpu_seconds or len(times) >= 5:
+                break
+        med = statistics.median(times)
+        ok = (np.array_equal(gpu_out[0], ref["accept_len"]) and
+              np.array_equal(gpu_out[1], ref["next_token"]) and
+              np.array_equal(gpu_out[2].view(np.uint32), ref["budget"].view(np.uint32)))
+        parity = "bit-exact" if ok else "MISMATCH"
+        cpu = {"value": w.rows_per_call / med, "unit": "rows/s", "cores": 1, "kind": "oracle",
+               "sample": "the full workload (%d rows x %d %s) verified %d times by the "
+                         "single-threaded C oracle, median %.2fs" % (
+                             w.rows_per_call, w.vocab, w.dtype, len(times), med)}
+        log("oracle: %.2fs per call (median of %d), parity %s" % (med, len(times), parity))
+
+    tag = "b%d_k%s_v%d_%s" % (w.num_requests, "16" if args.config in (2, 3) else
+                              ("32" if args.config == 4 else "1to8"), w.vocab, w.dtype)
+    traffic = read_traffic(tag, kernel_source_hash())
+    out = {
+        "metric": METRIC,
+        "value": rows_per_s,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded N(0,2^2) logits with a planted greedy peak; no datasets "
+                "or weights)",
+        "config": {"workload": "asd_verify %s: %d requests x (K=%s)+1 rows, V=%d %s, "
+                               "tau/cap/budgets per request" % (
+                                   w.name, w.num_requests,
+                                   "16" if args.config in (2, 3) else
+                                   ("32" if args.config == 4 else "1..8"),
+                                   w.vocab, w.dtype),
+                   "rows_per_call": w.rows_per_call, "vocab": w.vocab,
+                   "num_requests": w.num_requests,
+                   "logit_bytes_per_call": w.logit_bytes_per_call},
+        "achieved_GBps": achieved,
+        "parity": parity,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
+                     "algorithmic_bytes_per_launch": alg_bytes,
+                     "avg_launch_ms": avg_call_ms,
+                     "timing": "HIP events around every asd_verify call on its stream"},
+        "read_probe_GBps": probe_gbps,
+        "kernel_source_sha256_16": kernel_source_hash(),
+    }
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

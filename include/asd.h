@@ -1,0 +1,161 @@
+/*
+ * asd.h -- C ABI of the MI355X (gfx950) verifier of Approximate Speculative
+ * Decoding (ASD).
+ *
+ * One call verifies a batch of draft blocks against their teacher-forced
+ * target logits (Sec. 3.1, Eq. 1: row i of a block holds z_i =
+ * Target(h_0, x_{<i}); a block of K drafts has K + 1 rows, the last one giving
+ * the bonus token).  For every request it returns the longest feasible prefix
+ * of Algorithm 1 (Sec. 3.2, Eq. 12), the recovery or bonus token, and the
+ * updated regret ledger (Sec. 3.3, Eq. 13).
+ *
+ * Equations are numbered as in the paper: 1 target rows, 2 strict prefix,
+ * 3 local regret, 5 mismatch indicator, 6 remaining length q_i = K - i + 1,
+ * 7 normalized gate r_i / q_i <= g, 8 cumulative regret C_t and count N_t,
+ * 9 budget C_t <= B - s, 10 block cap N_t <= M, 11 gate at every accepted
+ * mismatch, 12 longest feasible prefix, 13 ledger update s' = s + C_a,
+ * 14 feasibility mask.
+ *
+ * All arrays are caller-owned device memory unless stated otherwise.  Every
+ * call is asynchronous on the given HIP stream (NULL = the null stream): it
+ * never synchronizes, and its outputs are valid in stream order.
+ */
+#ifndef ASD_H
+#define ASD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of the logits. */
+typedef enum {
+    ASD_F32 = 0,   /* IEEE binary32 */
+    ASD_BF16 = 1   /* bfloat16: the upper 16 bits of a binary32 value */
+} asd_dtype;
+
+typedef enum {
+    ASD_OK = 0,
+    ASD_EINVAL = 1,    /* an argument the host can check is invalid; nothing launched */
+    ASD_EDTYPE = 2,    /* unknown dtype; nothing launched */
+    ASD_ENOMEM = 3,    /* workspace could not be allocated, or too small */
+    ASD_EHIP = 4,      /* a HIP runtime call or kernel launch failed */
+    ASD_ECAPTURE = 5   /* the library workspace must grow while the stream is captured */
+} asd_status;
+
+/*
+ * Per-request regret ledger (B, s) (Sec. 3.2): total budget B and the regret s
+ * already spent by exceptions accepted in earlier rounds.  B = 0 selects exact
+ * greedy verification (Algorithm 1, first step; Eq. 2).
+ */
+typedef struct {
+    float total;   /* B */
+    float spent;   /* s, updated in place to s' (Eq. 13) */
+} asd_budget;
+
+/*
+ * asd_verify -- verify a batch of draft blocks (Algorithm 1 on every request).
+ *
+ * logits          [total_rows, vocab], row-major, dense, dtype elements; the
+ *                 base address must be a multiple of the element size.
+ * dtype           ASD_F32 or ASD_BF16.
+ * vocab           V, 1 <= V < 2^30.
+ * num_requests    number of requests (draft blocks) in the batch, >= 0;
+ *                 0 returns ASD_OK with nothing launched.
+ * total_rows      number of logit rows, num_requests <= total_rows < 2^31.
+ * draft_tokens    int32 [total_rows]: row o_i + p - 1 holds draft x_p of
+ *                 request i (p = 1..K_i); the entry of each bonus row o_i + K_i
+ *                 is ignored.
+ * block_lens      int32 [num_requests]: K_i >= 0.
+ * row_offsets     int64 [num_requests]: first row o_i of request i, or NULL for
+ *                 the packed layout o_i = sum_{j<i} (K_j + 1).
+ * tau             float [num_requests]: the local gate g_i of Eq. 7.
+ * exc_cap         int32 [num_requests]: the block cap M_i of Eq. 10
+ *                 (INT32_MAX acts as no cap).
+ * budget_inout    asd_budget [num_requests]: .total read, .spent read and
+ *                 rewritten (left bit-identical when no mismatch is accepted).
+ * out_accept_len  int32 [num_requests]: a_i in [0, K_i] (Eq. 12).
+ * out_next_token  int32 [num_requests]: y*_{a+1}, the recovery token when
+ *                 a_i < K_i and the bonus token y*_{K_i+1} when a_i = K_i.
+ * out_argmax      int32 [total_rows] or NULL: y* of every row (Eq. 1), the
+ *                 lowest index among equal greatest values.
+ * out_regret      float [total_rows] or NULL: for every row the regret of its
+ *                 draft entry, r = fl32(z(y*) - z(x)) (Eq. 3), +inf for an id
+ *                 outside [0, V); then +0 at the bonus row of every verified
+ *                 request.
+ * stream          a hipStream_t, or NULL.
+ *
+ * Semantics (bit-exact with the CPU oracle):
+ *  - argmax order: the numeric order with -0 == +0; a NaN with the sign bit
+ *    clear ranks above +inf and one with it set below -inf, NaNs of one sign
+ *    ordered by payload (IEEE 754 totalOrder).
+ *  - gate r_i <= g_i * q_i is decided exactly (binary64); budget as
+ *    fl32(s + C_t) <= B; cap as N_t <= M; C_t is a binary32 running sum in
+ *    position order; s' = fl32(s + C_a).
+ *  - B == 0 (either sign): exact greedy verification, ledger unchanged.
+ *  - a draft id outside [0, V) is a mismatch that is never accepted.
+ *  - a request with K_i < 0, o_i < 0 or o_i + K_i >= total_rows is not
+ *    verified: a_i = 0, next token = -1, ledger untouched.
+ *
+ * Outputs must not alias the inputs.  Calls that share the library workspace
+ * of one (device, stream) pair are ordered by the stream; calls on different
+ * streams use different workspaces.  The first call on a (device, stream)
+ * pair, or one that needs a larger workspace, allocates device memory
+ * (hipMalloc) and so must not happen during stream capture (ASD_ECAPTURE).
+ * Returns ASD_OK once the work is enqueued.
+ */
+asd_status asd_verify(const void *logits, asd_dtype dtype, int64_t vocab,
+                      int32_t num_requests, int64_t total_rows,
+                      const int32_t *draft_tokens, const int32_t *block_lens,
+                      const int64_t *row_offsets, const float *tau,
+                      const int32_t *exc_cap, asd_budget *budget_inout,
+                      int32_t *out_accept_len, int32_t *out_next_token,
+                      int32_t *out_argmax, float *out_regret, void *stream);
+
+/*
+ * asd_workspace_bytes -- device workspace that asd_verify_ws needs for a call
+ * of this shape on the current device.  Returns 0 for invalid arguments.
+ */
+size_t asd_workspace_bytes(asd_dtype dtype, int64_t vocab, int32_t num_requests,
+                           int64_t total_rows);
+
+/*
+ * asd_verify_ws -- asd_verify with a caller-provided workspace.
+ *
+ * workspace        device memory of at least asd_workspace_bytes(...) bytes,
+ *                  256-byte aligned.  Its first 16 KiB must hold zeros before
+ *                  its first use; every call leaves them zero again, so one
+ *                  workspace serves any later call of any shape (that fits)
+ *                  in stream order.  Calls that may overlap must use
+ *                  different workspaces.
+ * workspace_bytes  its size; too small returns ASD_ENOMEM with nothing launched.
+ * Never allocates, so it may be used during stream capture.
+ */
+asd_status asd_verify_ws(const void *logits, asd_dtype dtype, int64_t vocab,
+                         int32_t num_requests, int64_t total_rows,
+                         const int32_t *draft_tokens, const int32_t *block_lens,
+                         const int64_t *row_offsets, const float *tau,
+                         const int32_t *exc_cap, asd_budget *budget_inout,
+                         int32_t *out_accept_len, int32_t *out_next_token,
+                         int32_t *out_argmax, float *out_regret, void *stream,
+                         void *workspace, size_t workspace_bytes);
+
+/* Human-readable name of a status code (static storage). */
+const char *asd_status_string(asd_status status);
+
+/* Library version string, e.g. "asd-mi355x 0.1.0 gfx950" (static storage). */
+const char *asd_version(void);
+
+/*
+ * asd_release -- free every library-owned workspace.  The caller must make
+ * sure no enqueued asd_verify call is still running (synchronize first).
+ */
+asd_status asd_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ASD_H */

@@ -1,0 +1,175 @@
+"""MI355X (gfx950) verifier of Approximate Speculative Decoding.
+
+A thin ctypes binding over ``libasd.so`` (C ABI declared in ``include/asd.h``).
+The functions here only marshal torch tensors (device memory) and the current
+HIP stream into the C calls; every step of the verifier runs in the library's
+HIP kernels.  There is no CPU fallback: if the library is missing or a call
+fails, an exception is raised.
+"""
+import ctypes
+import os
+
+import torch
+
+from .build import LIBRARY
+
+__all__ = ["asd_verify", "asd_verify_ws", "asd_workspace_bytes", "asd_status_string",
+           "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16", "library_path"]
+
+ASD_F32 = 0
+ASD_BF16 = 1
+_DTYPES = {torch.float32: ASD_F32, torch.bfloat16: ASD_BF16}
+
+_lib = None
+
+
+class AsdError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = int(status)
+        super().__init__("%s failed: %s" % (where, asd_status_string(status)))
+
+
+def library_path() -> str:
+    return LIBRARY
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIBRARY):
+        raise RuntimeError("libasd.so is not built (%s); run __graft_entry__.build() first"
+                           % LIBRARY)
+    lib = ctypes.CDLL(LIBRARY)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    common = [vp, ctypes.c_int, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.asd_verify.argtypes = common
+    lib.asd_verify.restype = ctypes.c_int
+    lib.asd_verify_ws.argtypes = common + [vp, sz]
+    lib.asd_verify_ws.restype = ctypes.c_int
+    lib.asd_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i64]
+    lib.asd_workspace_bytes.restype = sz
+    lib.asd_status_string.argtypes = [ctypes.c_int]
+    lib.asd_status_string.restype = ctypes.c_char_p
+    lib.asd_version.argtypes = []
+    lib.asd_version.restype = ctypes.c_char_p
+    lib.asd_release.argtypes = []
+    lib.asd_release.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def asd_status_string(status) -> str:
+    return _load().asd_status_string(int(status)).decode()
+
+
+def asd_version() -> str:
+    return _load().asd_version().decode()
+
+
+def asd_release() -> None:
+    st = _load().asd_release()
+    if st != 0:
+        raise AsdError(st, "asd_release")
+
+
+def asd_workspace_bytes(dtype, vocab, num_requests, total_rows) -> int:
+    code = _DTYPES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return int(_load().asd_workspace_bytes(code, int(vocab), int(num_requests), int(total_rows)))
+
+
+def _per_request(value, n, dtype, device, name):
+    if isinstance(value, torch.Tensor):
+        if value.dtype != dtype or value.device != device or value.shape != (n,):
+            raise ValueError("%s must be a %s tensor of shape (%d,) on %s" % (name, dtype, n, device))
+        return value.contiguous()
+    return torch.full((n,), value, dtype=dtype, device=device)
+
+
+def _marshal(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets,
+             out_accept_len, out_next_token, out_argmax, out_regret):
+    if logits.dim() != 2 or logits.dtype not in _DTYPES or not logits.is_cuda:
+        raise ValueError("logits must be a 2-D float32 or bfloat16 tensor on a GPU")
+    if not logits.is_contiguous():
+        raise ValueError("logits must be contiguous (row-major, dense)")
+    dev = logits.device
+    rows, vocab = logits.shape
+    if block_lens.dtype != torch.int32 or block_lens.dim() != 1 or block_lens.device != dev:
+        raise ValueError("block_lens must be an int32 vector on the logits' device")
+    n = block_lens.shape[0]
+    if draft_tokens.dtype != torch.int32 or draft_tokens.shape != (rows,) or draft_tokens.device != dev:
+        raise ValueError("draft_tokens must be int32 of shape (%d,) on %s" % (rows, dev))
+    if budget.dtype != torch.float32 or budget.shape != (n, 2) or budget.device != dev \
+            or not budget.is_contiguous():
+        raise ValueError("budget must be a contiguous float32 (%d, 2) tensor on %s" % (n, dev))
+    if row_offsets is not None and (row_offsets.dtype != torch.int64 or row_offsets.shape != (n,)
+                                    or row_offsets.device != dev):
+        raise ValueError("row_offsets must be int64 of shape (%d,) on %s" % (n, dev))
+    tau = _per_request(tau, n, torch.float32, dev, "tau")
+    exc_cap = _per_request(exc_cap, n, torch.int32, dev, "exc_cap")
+    block_lens = block_lens.contiguous()
+    draft_tokens = draft_tokens.contiguous()
+    if out_accept_len is None:
+        out_accept_len = torch.empty(n, dtype=torch.int32, device=dev)
+    if out_next_token is None:
+        out_next_token = torch.empty(n, dtype=torch.int32, device=dev)
+    for t, name, shape, dt in ((out_accept_len, "out_accept_len", (n,), torch.int32),
+                               (out_next_token, "out_next_token", (n,), torch.int32),
+                               (out_argmax, "out_argmax", (rows,), torch.int32),
+                               (out_regret, "out_regret", (rows,), torch.float32)):
+        if t is not None and (t.dtype != dt or t.shape != shape or t.device != dev
+                              or not t.is_contiguous()):
+            raise ValueError("%s must be a contiguous %s tensor of shape %s on %s"
+                             % (name, dt, shape, dev))
+
+    def p(t):
+        return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    args = [p(logits), _DTYPES[logits.dtype], vocab, n, rows, p(draft_tokens), p(block_lens),
+            p(row_offsets), p(tau), p(exc_cap), p(budget), p(out_accept_len), p(out_next_token),
+            p(out_argmax), p(out_regret), ctypes.c_void_p(stream)]
+    keep = (tau, exc_cap, block_lens, draft_tokens)
+    return args, out_accept_len, out_next_token, keep
+
+
+def asd_verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, *, row_offsets=None,
+               out_accept_len=None, out_next_token=None, out_argmax=None, out_regret=None):
+    """Verify a batch of draft blocks on the GPU (``asd_verify`` of ``include/asd.h``).
+
+    logits        [total_rows, V] float32 or bfloat16, contiguous, on a GPU
+    draft_tokens  int32 [total_rows]
+    block_lens    int32 [num_requests] (K_i)
+    tau           float or float32 [num_requests]: local gate g of each request
+    exc_cap       int or int32 [num_requests]: block cap M of each request
+    budget        float32 [num_requests, 2] = (B, s); s is updated in place
+    Returns ``(accept_len, next_token)`` int32 tensors; the work is enqueued on
+    the current stream of the logits' device.
+    """
+    with torch.cuda.device(logits.device):
+        args, acc, nxt, keep = _marshal(logits, draft_tokens, block_lens, tau, exc_cap, budget,
+                                        row_offsets, out_accept_len, out_next_token,
+                                        out_argmax, out_regret)
+        st = _load().asd_verify(*args)
+    del keep
+    if st != 0:
+        raise AsdError(st, "asd_verify")
+    return acc, nxt
+
+
+def asd_verify_ws(logits, draft_tokens, block_lens, tau, exc_cap, budget, workspace, *,
+                  row_offsets=None, out_accept_len=None, out_next_token=None, out_argmax=None,
+                  out_regret=None):
+    """``asd_verify`` with a caller-provided workspace (a zero-initialised uint8 tensor)."""
+    if workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor")
+    with torch.cuda.device(logits.device):
+        args, acc, nxt, keep = _marshal(logits, draft_tokens, block_lens, tau, exc_cap, budget,
+                                        row_offsets, out_accept_len, out_next_token,
+                                        out_argmax, out_regret)
+        st = _load().asd_verify_ws(*args, ctypes.c_void_p(workspace.data_ptr()),
+                                   workspace.numel())
+    del keep
+    if st != 0:
+        raise AsdError(st, "asd_verify_ws")
+    return acc, nxt

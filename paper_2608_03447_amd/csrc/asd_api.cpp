@@ -1,0 +1,264 @@
+// C ABI of the ASD verifier: host-side argument checks, the launch plan, and
+// the library-owned per-(device, stream) workspaces.  Kernels are in
+// asd_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "../../include/asd.h"
+#include "asd_plan.h"
+
+namespace asd {
+
+namespace {
+
+size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
+
+// Tiles the row kernel aims for: enough resident workgroups to keep every
+// compute unit streaming, given 8 resident 256-thread workgroups per CU.
+constexpr int kTilesPerCu = 8;
+// Smallest split worth its own workgroup (vectors of 16 bytes = 16 KiB).
+constexpr int64_t kMinChunkVecs = 1024;
+
+}  // namespace
+
+Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int num_cus) {
+    Plan p{};
+    p.elem_bytes = elem_bytes;
+    p.vocab = vocab;
+    p.rows = rows;
+    const int64_t nvec_max = vocab * elem_bytes / 16;
+    int64_t splits = 1;
+    if (rows > 0 && rows <= kCounterSlots) {
+        const int64_t want = ((int64_t)num_cus * kTilesPerCu + rows - 1) / rows;
+        const int64_t most = nvec_max / kMinChunkVecs;
+        splits = want < most ? want : most;
+        if (splits > kMaxSplits) splits = kMaxSplits;
+        if (splits < 1) splits = 1;
+    }
+    int64_t chunk = (nvec_max + splits - 1) / splits;
+    chunk = (chunk + kRowThreads - 1) / kRowThreads * kRowThreads;
+    if (chunk < kRowThreads) chunk = kRowThreads;
+    splits = (nvec_max + chunk - 1) / chunk;
+    if (splits < 1) splits = 1;
+    p.splits = (int)splits;
+    p.chunk_vecs = chunk;
+
+    size_t off = 0;
+    p.off_counters = off;
+    off = align_up(off + (size_t)kCounterSlots * sizeof(int32_t), 256);
+    p.off_records = off;
+    off = align_up(off + (size_t)rows * sizeof(RowRecord), 256);
+    p.off_partials = off;
+    if (p.splits > 1) off = align_up(off + (size_t)rows * p.splits * sizeof(TilePartial), 256);
+    p.ws_bytes = off;
+    return p;
+}
+
+namespace {
+
+struct Workspace {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+};
+
+std::mutex g_mutex;
+std::map<std::pair<int, hipStream_t>, Workspace> g_workspaces;
+std::map<int, int> g_cu_count;
+
+asd_status cu_count(int device, int* out) {
+    auto it = g_cu_count.find(device);
+    if (it != g_cu_count.end()) {
+        *out = it->second;
+        return ASD_OK;
+    }
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+        n <= 0)
+        return ASD_EHIP;
+    g_cu_count[device] = n;
+    *out = n;
+    return ASD_OK;
+}
+
+int elem_bytes_of(asd_dtype dtype) {
+    switch (dtype) {
+        case ASD_F32: return 4;
+        case ASD_BF16: return 2;
+        default: return 0;
+    }
+}
+
+// Checks every argument the host can see; nothing is launched on failure.
+asd_status check_args(const void* logits, asd_dtype dtype, int64_t vocab, int32_t num_requests,
+                      int64_t total_rows, const int32_t* draft_tokens, const int32_t* block_lens,
+                      const float* tau, const int32_t* exc_cap, const asd_budget* budget,
+                      const int32_t* out_accept_len, const int32_t* out_next_token) {
+    const int eb = elem_bytes_of(dtype);
+    if (eb == 0) return ASD_EDTYPE;
+    if (vocab < 1 || vocab >= ((int64_t)1 << 30)) return ASD_EINVAL;
+    if (num_requests < 0 || total_rows < (int64_t)num_requests) return ASD_EINVAL;
+    if (total_rows >= ((int64_t)1 << 31)) return ASD_EINVAL;
+    if (num_requests == 0) return ASD_OK;
+    if (!logits || !draft_tokens || !block_lens || !tau || !exc_cap || !budget ||
+        !out_accept_len || !out_next_token)
+        return ASD_EINVAL;
+    if (((uintptr_t)logits % (uintptr_t)eb) != 0) return ASD_EINVAL;
+    if (total_rows > INT64_MAX / vocab / eb) return ASD_EINVAL;
+    return ASD_OK;
+}
+
+asd_status enqueue(const void* logits, asd_dtype dtype, int64_t vocab, int32_t num_requests,
+                   int64_t total_rows, const int32_t* draft_tokens, const int32_t* block_lens,
+                   const int64_t* row_offsets, const float* tau, const int32_t* exc_cap,
+                   asd_budget* budget, int32_t* out_accept_len, int32_t* out_next_token,
+                   int32_t* out_argmax, float* out_regret, hipStream_t stream, const Plan& plan,
+                   void* workspace) {
+    CallArgs a;
+    a.logits = logits;
+    a.num_requests = num_requests;
+    a.draft_tokens = draft_tokens;
+    a.block_lens = block_lens;
+    a.row_offsets = row_offsets;
+    a.tau = tau;
+    a.exc_cap = exc_cap;
+    a.budget = reinterpret_cast<float2*>(budget);
+    a.out_accept_len = out_accept_len;
+    a.out_next_token = out_next_token;
+    a.out_argmax = out_argmax;
+    a.out_regret = out_regret;
+    (void)dtype;
+    (void)vocab;
+    (void)total_rows;
+    return launch_verify(plan, a, workspace, stream) == hipSuccess ? ASD_OK : ASD_EHIP;
+}
+
+asd_status plan_for(asd_dtype dtype, int64_t vocab, int64_t total_rows, Plan* plan) {
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return ASD_EHIP;
+    int cus = 0;
+    asd_status st;
+    {
+        std::lock_guard<std::mutex> lock(g_mutex);
+        st = cu_count(device, &cus);
+    }
+    if (st != ASD_OK) return st;
+    *plan = make_plan(elem_bytes_of(dtype), vocab, total_rows, cus);
+    if ((int64_t)plan->rows * plan->splits >= ((int64_t)1 << 31)) return ASD_EINVAL;
+    return ASD_OK;
+}
+
+}  // namespace
+}  // namespace asd
+
+using namespace asd;
+
+extern "C" {
+
+asd_status asd_verify(const void* logits, asd_dtype dtype, int64_t vocab, int32_t num_requests,
+                      int64_t total_rows, const int32_t* draft_tokens, const int32_t* block_lens,
+                      const int64_t* row_offsets, const float* tau, const int32_t* exc_cap,
+                      asd_budget* budget_inout, int32_t* out_accept_len,
+                      int32_t* out_next_token, int32_t* out_argmax, float* out_regret,
+                      void* stream) {
+    asd_status st = check_args(logits, dtype, vocab, num_requests, total_rows, draft_tokens,
+                               block_lens, tau, exc_cap, budget_inout, out_accept_len,
+                               out_next_token);
+    if (st != ASD_OK || num_requests == 0) return st;
+    Plan plan;
+    if ((st = plan_for(dtype, vocab, total_rows, &plan)) != ASD_OK) return st;
+
+    hipStream_t s = (hipStream_t)stream;
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return ASD_EHIP;
+    void* ws = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_mutex);
+        Workspace& w = g_workspaces[std::make_pair(device, s)];
+        if (w.bytes < plan.ws_bytes) {
+            hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+            if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ASD_EHIP;
+            if (cap != hipStreamCaptureStatusNone) return ASD_ECAPTURE;
+            size_t want = plan.ws_bytes;
+            if (want < (size_t)1 << 20) want = (size_t)1 << 20;
+            want = align_up(want, (size_t)1 << 20);
+            if (w.ptr) {
+                if (hipStreamSynchronize(s) != hipSuccess) return ASD_EHIP;
+                (void)hipFree(w.ptr);
+                w.ptr = nullptr;
+                w.bytes = 0;
+            }
+            void* p = nullptr;
+            if (hipMalloc(&p, want) != hipSuccess) return ASD_ENOMEM;
+            if (hipMemsetAsync(p, 0, want, s) != hipSuccess) {
+                (void)hipFree(p);
+                return ASD_EHIP;
+            }
+            w.ptr = p;
+            w.bytes = want;
+        }
+        ws = w.ptr;
+    }
+    return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
+                   row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
+                   out_argmax, out_regret, s, plan, ws);
+}
+
+size_t asd_workspace_bytes(asd_dtype dtype, int64_t vocab, int32_t num_requests,
+                           int64_t total_rows) {
+    if (elem_bytes_of(dtype) == 0 || vocab < 1 || vocab >= ((int64_t)1 << 30) ||
+        num_requests < 0 || total_rows < (int64_t)num_requests ||
+        total_rows >= ((int64_t)1 << 31))
+        return 0;
+    Plan plan;
+    if (plan_for(dtype, vocab, total_rows, &plan) != ASD_OK) return 0;
+    return plan.ws_bytes;
+}
+
+asd_status asd_verify_ws(const void* logits, asd_dtype dtype, int64_t vocab,
+                         int32_t num_requests, int64_t total_rows, const int32_t* draft_tokens,
+                         const int32_t* block_lens, const int64_t* row_offsets, const float* tau,
+                         const int32_t* exc_cap, asd_budget* budget_inout,
+                         int32_t* out_accept_len, int32_t* out_next_token, int32_t* out_argmax,
+                         float* out_regret, void* stream, void* workspace,
+                         size_t workspace_bytes) {
+    asd_status st = check_args(logits, dtype, vocab, num_requests, total_rows, draft_tokens,
+                               block_lens, tau, exc_cap, budget_inout, out_accept_len,
+                               out_next_token);
+    if (st != ASD_OK || num_requests == 0) return st;
+    if (!workspace || ((uintptr_t)workspace & 255) != 0) return ASD_EINVAL;
+    Plan plan;
+    if ((st = plan_for(dtype, vocab, total_rows, &plan)) != ASD_OK) return st;
+    if (workspace_bytes < plan.ws_bytes) return ASD_ENOMEM;
+    return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
+                   row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
+                   out_argmax, out_regret, (hipStream_t)stream, plan, workspace);
+}
+
+const char* asd_status_string(asd_status status) {
+    switch (status) {
+        case ASD_OK: return "ASD_OK";
+        case ASD_EINVAL: return "ASD_EINVAL: invalid argument";
+        case ASD_EDTYPE: return "ASD_EDTYPE: unknown logits dtype";
+        case ASD_ENOMEM: return "ASD_ENOMEM: workspace allocation failed or too small";
+        case ASD_EHIP: return "ASD_EHIP: HIP runtime error";
+        case ASD_ECAPTURE: return "ASD_ECAPTURE: workspace must grow during stream capture";
+        default: return "ASD: unknown status";
+    }
+}
+
+const char* asd_version(void) { return "asd-mi355x 0.1.0 gfx950"; }
+
+asd_status asd_release(void) {
+    std::lock_guard<std::mutex> lock(g_mutex);
+    asd_status st = ASD_OK;
+    for (auto& kv : g_workspaces) {
+        if (kv.second.ptr && hipFree(kv.second.ptr) != hipSuccess) st = ASD_EHIP;
+    }
+    g_workspaces.clear();
+    return st;
+}
+
+}  // extern "C"

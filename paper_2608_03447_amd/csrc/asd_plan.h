@@ -1,0 +1,80 @@
+// Launch plan and workspace layout shared by the C-ABI host code and the
+// gfx950 kernels of the ASD verifier.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace asd {
+
+// Threads per workgroup of the row kernel: four 64-wide wavefronts.
+constexpr int kRowThreads = 256;
+// Threads of the per-request scan kernel.
+constexpr int kScanThreads = 256;
+// Largest number of vocabulary splits of one row.
+constexpr int kMaxSplits = 64;
+// Per-row completion counters live in a fixed region at the start of every
+// workspace, whatever the call's shape, so that no other shape's data ever
+// lands on them.  Rows are split over several workgroups only when there are
+// at most this many rows.
+constexpr int kCounterSlots = 4096;
+
+// One tile's best candidate: (key, column) packed so that a larger value means
+// a greater logit, and among equal logits a lower column; plus the logit's
+// binary32 bit pattern and the gathered draft logit when the tile owns it.
+struct alignas(16) TilePartial {
+    unsigned long long packed;
+    uint32_t bits;
+    uint32_t draft_bits;
+};
+
+// Per-row result consumed by the per-request scan: argmax in the low 30 bits,
+// bit 31 = mismatch (draft != argmax), bit 30 = draft id outside [0, V);
+// and the regret r = fl32(z(y*) - z(x)).
+struct alignas(8) RowRecord {
+    uint32_t y_flags;
+    float regret;
+};
+
+constexpr uint32_t kMismatchBit = 0x80000000u;
+constexpr uint32_t kBadDraftBit = 0x40000000u;
+constexpr uint32_t kArgmaxMask = 0x3fffffffu;
+
+struct Plan {
+    int elem_bytes;          // 2 (bf16) or 4 (f32)
+    int64_t vocab;
+    int64_t rows;
+    int splits;              // S >= 1 vocabulary splits per row
+    int64_t chunk_vecs;      // 16-byte vectors per split (multiple of kRowThreads)
+    // Workspace layout (byte offsets from the workspace base; 256-byte aligned):
+    // [0, kCounterSlots * 4) completion counters, zero between calls;
+    // then the row records; then the split partials (splits > 1 only).
+    size_t off_counters;
+    size_t off_records;
+    size_t off_partials;
+    size_t ws_bytes;
+};
+
+// Arguments of one verifier call after host validation.
+struct CallArgs {
+    const void* logits;
+    int32_t num_requests;
+    const int32_t* draft_tokens;
+    const int32_t* block_lens;
+    const int64_t* row_offsets;
+    const float* tau;
+    const int32_t* exc_cap;
+    float2* budget;          // (B, s) per request
+    int32_t* out_accept_len;
+    int32_t* out_next_token;
+    int32_t* out_argmax;
+    float* out_regret;
+};
+
+Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int num_cus);
+
+hipError_t launch_verify(const Plan& plan, const CallArgs& args, void* workspace,
+                         hipStream_t stream);
+
+}  // namespace asd

@@ -1,0 +1,90 @@
+"""The C-ABI library: it loads, exports every function include/asd.h declares,
+and rejects invalid host-checkable arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_03447_amd as asd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "asd.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(asd_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("asd_verify", "asd_verify_ws", "asd_workspace_bytes", "asd_status_string",
+              "asd_version", "asd_release"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(asd.library_path())
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version():
+    assert asd.asd_status_string(0) == "ASD_OK"
+    assert "EINVAL" in asd.asd_status_string(1)
+    assert "unknown" in asd.asd_status_string(99)
+    assert "gfx950" in asd.asd_version()
+
+
+def _call(**kw):
+    lib = asd._load()
+    a = dict(logits=0x1000, dtype=1, vocab=100, nreq=1, rows=2, draft=0x2000, lens=0x3000,
+             offs=None, tau=0x4000, cap=0x5000, budget=0x6000, acc=0x7000, nxt=0x8000,
+             amax=None, regret=None, stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_verify(vp(a["logits"]), a["dtype"], a["vocab"], a["nreq"], a["rows"],
+                          vp(a["draft"]), vp(a["lens"]), vp(a["offs"]), vp(a["tau"]),
+                          vp(a["cap"]), vp(a["budget"]), vp(a["acc"]), vp(a["nxt"]),
+                          vp(a["amax"]), vp(a["regret"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), 2),
+    (dict(vocab=0), 1),
+    (dict(vocab=1 << 30), 1),
+    (dict(nreq=-1), 1),
+    (dict(nreq=3, rows=2), 1),
+    (dict(rows=1 << 31), 1),
+    (dict(logits=None), 1),
+    (dict(draft=None), 1),
+    (dict(lens=None), 1),
+    (dict(tau=None), 1),
+    (dict(cap=None), 1),
+    (dict(budget=None), 1),
+    (dict(acc=None), 1),
+    (dict(nxt=None), 1),
+    (dict(logits=0x1001), 1),                  # not a multiple of the bf16 size
+    (dict(dtype=0, logits=0x1002), 1),         # not a multiple of the f32 size
+])
+def test_invalid_arguments_are_rejected_without_launch(kw, status):
+    assert _call(**kw) == status
+
+
+def test_empty_batch_is_a_no_op():
+    assert _call(nreq=0, rows=0, logits=None, draft=None) == 0
+
+
+def test_workspace_bytes_rejects_invalid_shapes():
+    lib = asd._load()
+    assert lib.asd_workspace_bytes(9, 100, 1, 2) == 0
+    assert lib.asd_workspace_bytes(1, 0, 1, 2) == 0
+    assert lib.asd_workspace_bytes(1, 100, 3, 2) == 0
+
+
+def test_package_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(asd, "_lib", None)
+    monkeypatch.setattr(asd, "LIBRARY", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        asd._load()
