@@ -81,10 +81,10 @@ typedef struct {
  *                 a_i < K_i and the bonus token y*_{K_i+1} when a_i = K_i.
  * out_argmax      int32 [total_rows] or NULL: y* of every row (Eq. 1), the
  *                 lowest index among equal greatest values.
- * out_regret      float [total_rows] or NULL: for every row the regret of its
- *                 draft entry, r = fl32(z(y*) - z(x)) (Eq. 3), +inf for an id
- *                 outside [0, V); then +0 at the bonus row of every verified
- *                 request.
+ * out_regret      float [total_rows] or NULL: for the rows of every verified
+ *                 request, r = fl32(z(y*) - z(x)) (Eq. 3) at each draft row
+ *                 (+inf for an id outside [0, V)) and +0 at its bonus row.
+ *                 Rows outside verified requests are not written.
  * stream          a hipStream_t, or NULL.
  *
  * Semantics (bit-exact with the CPU oracle):
@@ -125,11 +125,10 @@ size_t asd_workspace_bytes(asd_dtype dtype, int64_t vocab, int32_t num_requests,
  * asd_verify_ws -- asd_verify with a caller-provided workspace.
  *
  * workspace        device memory of at least asd_workspace_bytes(...) bytes,
- *                  256-byte aligned.  Its first 16 KiB must hold zeros before
- *                  its first use; every call leaves them zero again, so one
- *                  workspace serves any later call of any shape (that fits)
- *                  in stream order.  Calls that may overlap must use
- *                  different workspaces.
+ *                  256-byte aligned, with any content: nothing in it is
+ *                  carried between calls, so one workspace serves any later
+ *                  call that fits, in stream order.  Calls that may overlap
+ *                  must use different workspaces.
  * workspace_bytes  its size; too small returns ASD_ENOMEM with nothing launched.
  * Never allocates, so it may be used during stream capture.
  */

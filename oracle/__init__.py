@@ -99,7 +99,7 @@ def verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets=N
     ``budget`` is a float32 [B, 2] array of (total, spent); a new array with the
     updated ledger is returned (the input is not modified).
     Returns a dict with ``accept_len``, ``next_token``, ``budget``, ``argmax``,
-    ``regret`` (every row's draft regret; +0 at bonus rows of verified requests).
+    ``regret`` (rows outside verified requests hold NaN).
     """
     logits = np.ascontiguousarray(logits)
     code = _dtype_code(logits)

@@ -42,10 +42,9 @@
  *   - the B = 0 dispatch tests the total budget B (so -0 counts as zero).
  *   - a draft id outside [0, V) is a mismatch that is never feasible, with
  *     r = +inf.
- *   - the bonus row's draft entry is ignored by the scan.  The per-row regret
- *     output holds, for every row, the regret of that row's draft entry
- *     (+inf for an id outside [0, V)); the bonus row of every verified
- *     request then holds +0.
+ *   - the bonus row's draft entry is ignored.  The per-row regret output is
+ *     written for the rows of verified requests only: r_i at draft rows, +0
+ *     at the bonus row.
  *   - a request whose rows do not fit in [0, total_rows) or whose K is
  *     negative is not verified: a = 0, next token = -1, state untouched.
  *
@@ -234,9 +233,8 @@ void oracle_block(int32_t K, const int32_t *x, const uint8_t *x_valid,
  * budget        [num_requests][2] = (B, s); s updated in place
  * out_accept_len, out_next_token [num_requests]
  * out_argmax    [total_rows] or NULL: y* of every row
- * out_regret    [total_rows] or NULL: for every row the regret of its draft
- *               entry (Eq. 3; +inf for an id outside [0, V)), then +0 at the
- *               bonus row of every verified request
+ * out_regret    [total_rows] or NULL: r of every draft row of a verified
+ *               request, +0 for its bonus row; other rows are not written
  * Returns 0, or 1 for an argument the call cannot work with.
  */
 int oracle_verify(const void *logits, int dtype, int64_t vocab,
@@ -259,13 +257,6 @@ int oracle_verify(const void *logits, int dtype, int64_t vocab,
         y_all[row] = (int32_t)oracle_row_argmax(logits, dtype, vocab, row);
         if (out_argmax)
             out_argmax[row] = y_all[row];
-        if (out_regret) {
-            int32_t x = draft[row];
-            out_regret[row] = (x >= 0 && (int64_t)x < vocab)
-                ? logit_at(logits, dtype, vocab, row, y_all[row]) -
-                  logit_at(logits, dtype, vocab, row, x)
-                : INFINITY;
-        }
     }
 
     for (int32_t i = 0; i < num_requests; ++i) {
@@ -303,8 +294,11 @@ int oracle_verify(const void *logits, int dtype, int64_t vocab,
             budget[2 * i + 1] = s;
             out_accept_len[i] = a;
             out_next_token[i] = next;
-            if (out_regret)
+            if (out_regret) {
+                for (int32_t p = 0; p < K; ++p)
+                    out_regret[o + p] = r[p];
                 out_regret[o + K] = 0.0f;
+            }
             free(x);
             free(x_valid);
             free(z_y);

@@ -5,17 +5,22 @@
 // keeps, per lane, the greatest logit seen so far (Eq. 1).  Logits are compared
 // as order-preserving integer keys, so the whole reduction is integer max work
 // with no rounding.  The tile that owns the draft token's column also gathers
-// z(x) (Eq. 3).  The last tile of a row to finish combines the split partials,
-// forms the regret r = fl32(z(y*) - z(x)) and the mismatch bit d (Eq. 5), and
-// writes the row's record.
+// z(x) (Eq. 3).  With one tile per row the tile writes the row's record:
+// argmax, mismatch bit d (Eq. 5) and regret r = fl32(z(y*) - z(x)).  With
+// several tiles per row each tile writes a partial; no workgroup waits for or
+// signals another.  Block 0 also writes the packed row offsets of the requests.
 //
-// Stage 2 (asd_scan_kernel): one thread per request runs Algorithm 1 over the
-// row records of its block: the B = 0 dispatch to exact greedy verification
-// (Eq. 2), otherwise the left-to-right scan that accepts a mismatch only while
-// the gate r <= g q (Eqs. 7, 11), the budget fl32(s + C) <= B (Eq. 9) and the
-// cap N <= M (Eq. 10) hold, stopping at the first infeasible position (the
-// longest feasible prefix, Eq. 12); then the ledger update (Eq. 13) and the
-// recovery or bonus token.
+// Stage 2 (asd_scan_kernel): one wavefront per request runs Algorithm 1 with
+// lanes = block positions.  Each lane forms its row's record (or combines the
+// row's split partials), then the wavefront ballots the mismatches and walks
+// only those, in position order: the B = 0 dispatch stops at the first one
+// (Eq. 2); otherwise a mismatch is accepted while the gate r <= g q (Eqs. 7,
+// 11), the budget fl32(s + C) <= B (Eq. 9) and the cap N <= M (Eq. 10) hold,
+// and the first that fails ends the longest feasible prefix (Eq. 12).  Exact
+// matches in between are feasible by Eq. 14's first term.  The running sum C
+// is accumulated in position order, one binary32 addition per accepted
+// mismatch, exactly as the sequential definition does.  Then the ledger update
+// (Eq. 13) and the recovery or bonus token.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -176,14 +181,12 @@ struct RowGeom {
     int64_t head, nvec, tail;
 };
 
-template <int EB>
-__device__ __forceinline__ RowGeom row_geom(const unsigned char* row_ptr, int64_t vocab) {
-    constexpr int kEpv = 16 / EB;
+__device__ __forceinline__ RowGeom row_geom(const unsigned char* row_ptr, int64_t vocab, int eb) {
     RowGeom g;
-    const int64_t mis = (int64_t)((16 - ((uintptr_t)row_ptr & 15)) & 15) / EB;
+    const int64_t mis = (int64_t)((16 - ((uintptr_t)row_ptr & 15)) & 15) / eb;
     g.head = mis < vocab ? mis : vocab;
-    g.nvec = (vocab - g.head) / kEpv;
-    g.tail = g.head + g.nvec * kEpv;
+    g.nvec = (vocab - g.head) * eb / 16;
+    g.tail = g.head + g.nvec * (16 / eb);
     return g;
 }
 
@@ -195,20 +198,55 @@ __device__ __forceinline__ int owner_split(int64_t c, const RowGeom& g, int64_t 
     return s < splits - 1 ? (int)s : splits - 1;
 }
 
+// Packed layout o_i = sum_{j<i} (max(K_j, 0) + 1), written by one workgroup:
+// an exclusive scan of the row counts in chunks of kRowThreads requests.
+__device__ void write_packed_offsets(int32_t num_requests, const int32_t* __restrict__ block_lens,
+                                     int64_t* __restrict__ offsets) {
+    __shared__ long long s_wave[kWaves];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    long long carry = 0;
+    for (int64_t c0 = 0; c0 < num_requests; c0 += kRowThreads) {
+        const int64_t i = c0 + tid;
+        const int32_t K = i < num_requests ? block_lens[i] : 0;
+        const long long n = i < num_requests ? (long long)(K > 0 ? K : 0) + 1 : 0;
+        long long incl = n;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const long long t = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += t;
+        }
+        if (lane == 63) s_wave[wave] = incl;
+        __syncthreads();
+        long long before = 0, chunk_total = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const long long t = s_wave[w];
+            before += (w < wave) ? t : 0;
+            chunk_total += t;
+        }
+        __syncthreads();
+        if (i < num_requests) offsets[i] = carry + before + incl - n;
+        carry += chunk_total;
+    }
+}
+
 // ----------------------------------------------------------- stage 1 kernel
 
 template <int EB>
 __global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
     const unsigned char* __restrict__ logits, int64_t vocab, int splits, int64_t chunk_vecs,
     const int32_t* __restrict__ draft_tokens, TilePartial* __restrict__ partials,
-    int32_t* __restrict__ row_counters, RowRecord* __restrict__ records,
-    int32_t* __restrict__ out_argmax, float* __restrict__ out_regret) {
+    RowRecord* __restrict__ records, int32_t* __restrict__ out_argmax, int32_t num_requests,
+    const int32_t* __restrict__ block_lens, int64_t* __restrict__ packed_offsets) {
     constexpr int kEpv = 16 / EB;
     const int tid = threadIdx.x;
+    if (packed_offsets != nullptr && blockIdx.x == 0)
+        write_packed_offsets(num_requests, block_lens, packed_offsets);
+
     const int64_t row = blockIdx.x / splits;
     const int split = (int)(blockIdx.x - row * splits);
     const unsigned char* row_ptr = logits + row * vocab * EB;
-    const RowGeom geom = row_geom<EB>(row_ptr, vocab);
+    const RowGeom geom = row_geom(row_ptr, vocab, EB);
     const int64_t chunk_cols = chunk_vecs * kEpv;
 
     // Draft token of this row (uniform); the owning tile gathers z(x) early so
@@ -313,177 +351,180 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
     block_reduce(packed, bits);
     if (tid != 0) return;
 
-    // ---- combine the splits of this row (the last tile to finish does it)
-    if (splits > 1) {
-        TilePartial* mine = partials + row * splits;
+    if (splits > 1) {                    // combined by the scan kernel
         TilePartial tp;
         tp.packed = packed;
         tp.bits = bits;
-        tp.draft_bits = draft_bits;
-        mine[split] = tp;
-        const int32_t done = __hip_atomic_fetch_add(row_counters + row, 1, __ATOMIC_ACQ_REL,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-        if (done != splits - 1) return;
-        row_counters[row] = 0;            // ready for the next call
-        if (x_valid) draft_bits = mine[owner_split(x, geom, chunk_cols, splits)].draft_bits;
-        for (int s = 0; s < splits; ++s) {
-            if (s == split) continue;
-            const TilePartial o = mine[s];
-            take_better(packed, bits, o.packed, o.bits);
-        }
+        tp.draft_bits = draft_bits;      // meaningful in the owning tile only
+        partials[blockIdx.x] = tp;
+        return;
     }
 
-    // ---- row record: argmax, mismatch bit, regret (one binary32 subtraction)
+    // ---- one tile per row: the row record (one binary32 subtraction)
     const int32_t y = packed_col(packed);
-    float r;
-    uint32_t flags;
-    if (x_valid) {
-        r = bits_to_float(bits) - bits_to_float(draft_bits);
-        flags = (x != y) ? kMismatchBit : 0u;
-    } else {
-        r = __builtin_huge_valf();
-        flags = kMismatchBit | kBadDraftBit;
-    }
     RowRecord rec;
-    rec.y_flags = (uint32_t)y | flags;
-    rec.regret = r;
+    if (x_valid) {
+        rec.regret = bits_to_float(bits) - bits_to_float(draft_bits);
+        rec.y_flags = (uint32_t)y | ((x != y) ? kMismatchBit : 0u);
+    } else {
+        rec.regret = __builtin_huge_valf();
+        rec.y_flags = (uint32_t)y | kMismatchBit | kBadDraftBit;
+    }
     records[row] = rec;
     if (out_argmax) out_argmax[row] = y;
-    if (out_regret) out_regret[row] = r;
 }
 
 // ----------------------------------------------------------- stage 2 kernel
 
-// Records read ahead per scan window: one window covers K <= 31 and the bonus row.
-constexpr int kScanWindow = 32;
+struct ScanArgs {
+    int32_t num_requests;
+    int32_t request_blocks;      // workgroups that scan requests; the rest write argmax rows
+    int64_t total_rows;
+    int64_t vocab;
+    int elem_bytes;
+    int splits;
+    int64_t chunk_vecs;
+    const unsigned char* logits; // row addresses only (alignment -> split ownership)
+    const int32_t* draft_tokens;
+    const int32_t* block_lens;
+    const int64_t* offsets;
+    const float* tau;
+    const int32_t* exc_cap;
+    float2* budget;
+    const RowRecord* records;    // splits == 1
+    const TilePartial* partials; // splits > 1
+    int32_t* out_accept_len;
+    int32_t* out_next_token;
+    float* out_regret;
+    int32_t* out_argmax;
+};
 
-// Algorithm 1 for request i whose rows start at o (validated by the caller).
-__device__ __forceinline__ void scan_request(int32_t i, int64_t o, int32_t K, const float* tau,
-                                             const int32_t* exc_cap, float2* budget,
-                                             const RowRecord* records, int32_t* out_accept_len,
-                                             int32_t* out_next_token, float* out_regret) {
-    const float2 ledger = budget[i];
+// Greatest (key, column) of a row's split partials and the gathered draft logit.
+__device__ __forceinline__ void combine_row(const ScanArgs& A, int64_t row, int32_t x,
+                                            unsigned long long& packed, uint32_t& bits,
+                                            uint32_t& draft_bits) {
+    const TilePartial* parts = A.partials + row * A.splits;
+    const unsigned char* row_ptr = A.logits + row * A.vocab * A.elem_bytes;
+    const RowGeom geom = row_geom(row_ptr, A.vocab, A.elem_bytes);
+    const int owner = (x >= 0 && (int64_t)x < A.vocab)
+                          ? owner_split(x, geom, A.chunk_vecs * (16 / A.elem_bytes), A.splits)
+                          : -1;
+    packed = 0;
+    bits = 0;
+    draft_bits = 0;
+    for (int s = 0; s < A.splits; ++s) {
+        const TilePartial tp = parts[s];
+        take_better(packed, bits, tp.packed, tp.bits);
+        if (s == owner) draft_bits = tp.draft_bits;
+    }
+}
+
+__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int lane) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
+__global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+    if ((int32_t)blockIdx.x >= A.request_blocks) {
+        // Argmax of every row when rows were split (one lane per row).
+        const int64_t row = (int64_t)(blockIdx.x - A.request_blocks) * kScanThreads + tid;
+        if (row < A.total_rows) {
+            unsigned long long packed;
+            uint32_t bits, draft_bits;
+            combine_row(A, row, -1, packed, bits, draft_bits);
+            A.out_argmax[row] = packed_col(packed);
+        }
+        return;
+    }
+
+    const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
+    if (i >= A.num_requests) return;
+    const int32_t K = A.block_lens[i];
+    const int64_t o = A.offsets[i];
+    if (!(K >= 0 && o >= 0 && o + (int64_t)K < A.total_rows)) {
+        if (lane == 0) {
+            A.out_accept_len[i] = 0;
+            A.out_next_token[i] = -1;
+        }
+        return;
+    }
+    const float2 ledger = A.budget[i];
     const float B = ledger.x;
-    float s = ledger.y;
-    const float g = tau[i];
-    const int32_t M = exc_cap[i];
-    const bool strict = (B == 0.0f);      // Algorithm 1: B = 0 -> exact greedy verification
+    const float s = ledger.y;
+    const float g = A.tau[i];
+    const int32_t M = A.exc_cap[i];
+    const bool strict = (B == 0.0f);   // Algorithm 1: B = 0 -> exact greedy verification
 
     int32_t a = 0, N = 0, next = -1;
     float C = 0.0f;
-    bool stop = false;
-    for (int64_t w0 = 0; w0 <= K && !stop; w0 += kScanWindow) {
-        RowRecord rec[kScanWindow];
-#pragma unroll
-        for (int j = 0; j < kScanWindow; ++j)
-            if (w0 + j <= K) rec[j] = records[o + w0 + j];
-#pragma unroll
-        for (int j = 0; j < kScanWindow; ++j) {
-            const int64_t p = w0 + j;                 // 0-based position; p == K: bonus row
-            if (!stop && p <= K) {
-                const uint32_t yf = rec[j].y_flags;
-                bool accept = (p < K) && (yf & kMismatchBit) == 0u;   // exact match
-                if (p < K && !accept && !strict && (yf & kBadDraftBit) == 0u) {
-                    const float r = rec[j].regret;
-                    const int32_t q = K - (int32_t)p;  // q_i = K - i + 1 with i = p + 1
-                    const bool gate = (double)r <= (double)g * (double)q;
-                    const float C_new = C + r;
-                    const int32_t N_new = N + 1;
-                    const float s_new = s + C_new;
-                    if (gate && s_new <= B && N_new <= M) {
-                        C = C_new;
-                        N = N_new;
-                        accept = true;
-                    }
-                }
-                if (accept) {
-                    a = (int32_t)p + 1;
-                } else {
-                    // First infeasible position, or the bonus row after a
-                    // fully accepted block: emit y*_{a+1}.
-                    next = (int32_t)(yf & kArgmaxMask);
-                    stop = true;
-                }
-            }
-        }
-    }
-    if (N > 0) {
-        s = s + C;                                    // s' = s + C_a
-        budget[i].y = s;
-    }
-    out_accept_len[i] = a;
-    out_next_token[i] = next;
-    if (out_regret) out_regret[o + K] = 0.0f;
-}
-
-// Per-request validity: rows [o, o + K] inside [0, total_rows).
-__device__ __forceinline__ bool request_ok(int64_t o, int32_t K, int64_t total_rows) {
-    return K >= 0 && o >= 0 && o + (int64_t)K < total_rows;
-}
-
-// Requests with explicit row offsets: one thread per request, any grid.
-__global__ __launch_bounds__(kScanThreads) void asd_scan_offsets_kernel(
-    int32_t num_requests, int64_t total_rows, const int32_t* __restrict__ block_lens,
-    const int64_t* __restrict__ row_offsets, const float* __restrict__ tau,
-    const int32_t* __restrict__ exc_cap, float2* __restrict__ budget,
-    const RowRecord* __restrict__ records, int32_t* __restrict__ out_accept_len,
-    int32_t* __restrict__ out_next_token, float* __restrict__ out_regret) {
-    const int64_t i = (int64_t)blockIdx.x * kScanThreads + threadIdx.x;
-    if (i >= num_requests) return;
-    const int32_t K = block_lens[i];
-    const int64_t o = row_offsets[i];
-    if (!request_ok(o, K, total_rows)) {
-        out_accept_len[i] = 0;
-        out_next_token[i] = -1;
-        return;
-    }
-    scan_request((int32_t)i, o, K, tau, exc_cap, budget, records, out_accept_len, out_next_token,
-                 out_regret);
-}
-
-// Packed layout o_i = sum_{j<i} (max(K_j, 0) + 1): one workgroup walks the
-// requests in chunks, an exclusive scan of the row counts giving each offset.
-__global__ __launch_bounds__(kScanThreads) void asd_scan_packed_kernel(
-    int32_t num_requests, int64_t total_rows, const int32_t* __restrict__ block_lens,
-    const float* __restrict__ tau, const int32_t* __restrict__ exc_cap,
-    float2* __restrict__ budget, const RowRecord* __restrict__ records,
-    int32_t* __restrict__ out_accept_len, int32_t* __restrict__ out_next_token,
-    float* __restrict__ out_regret) {
-    __shared__ long long s_wave[kScanThreads / 64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    long long carry = 0;
-    for (int64_t c0 = 0; c0 < num_requests; c0 += kScanThreads) {
-        const int64_t i = c0 + tid;
-        const int32_t K = i < num_requests ? block_lens[i] : 0;
-        const long long n = i < num_requests ? (long long)(K > 0 ? K : 0) + 1 : 0;
-        // inclusive scan within the wavefront
-        long long incl = n;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const long long t = __shfl_up(incl, off, 64);
-            if (lane >= off) incl += t;
-        }
-        if (lane == 63) s_wave[wave] = incl;
-        __syncthreads();
-        long long before = 0, chunk_total = 0;
-#pragma unroll
-        for (int w = 0; w < kScanThreads / 64; ++w) {
-            const long long t = s_wave[w];
-            before += (w < wave) ? t : 0;
-            chunk_total += t;
-        }
-        __syncthreads();
-        const int64_t o = carry + before + incl - n;
-        carry += chunk_total;
-        if (i < num_requests) {
-            if (!request_ok(o, K, total_rows)) {
-                out_accept_len[i] = 0;
-                out_next_token[i] = -1;
+    bool done = false;
+    for (int64_t c0 = 0; c0 <= K; c0 += 64) {
+        const int64_t p = c0 + lane;                  // 0-based position; p == K: bonus row
+        const bool have = p <= K;
+        const bool is_draft = p < K;
+        uint32_t y = 0;
+        bool mism = false, bad = false;
+        float r = 0.0f;
+        if (have) {
+            const int64_t row = o + p;
+            if (A.splits == 1) {
+                const RowRecord rec = A.records[row];
+                y = rec.y_flags & kArgmaxMask;
+                mism = (rec.y_flags & kMismatchBit) != 0u;
+                bad = (rec.y_flags & kBadDraftBit) != 0u;
+                r = rec.regret;
             } else {
-                scan_request((int32_t)i, o, K, tau, exc_cap, budget, records, out_accept_len,
-                             out_next_token, out_regret);
+                const int32_t x = A.draft_tokens[row];
+                unsigned long long packed;
+                uint32_t bits, draft_bits;
+                combine_row(A, row, x, packed, bits, draft_bits);
+                y = (uint32_t)packed_col(packed);
+                bad = !(x >= 0 && (int64_t)x < A.vocab);
+                mism = bad || (uint32_t)x != y;
+                r = bad ? __builtin_huge_valf() : bits_to_float(bits) - bits_to_float(draft_bits);
+            }
+            if (A.out_regret) A.out_regret[row] = is_draft ? r : 0.0f;
+        }
+        if (done) continue;
+
+        // Mismatches among this chunk's draft positions, and those that pass
+        // the local gate r <= g q (q = K - p, i.e. K - i + 1 for i = p + 1).
+        const bool gate = (double)r <= (double)g * (double)(int32_t)(K - (int32_t)p);
+        const unsigned long long mism_mask = __ballot(is_draft && mism);
+        const unsigned long long ok_mask = __ballot(is_draft && mism && !bad && gate);
+        int stop = -1;
+        if (strict) {
+            if (mism_mask) stop = __builtin_ctzll(mism_mask);
+        } else {
+            for (unsigned long long m = mism_mask; m != 0ull; m &= m - 1ull) {
+                const int j = __builtin_ctzll(m);
+                const float rj = __builtin_bit_cast(float, lane_u32(__builtin_bit_cast(uint32_t, r), j));
+                const float C_new = C + rj;
+                const int32_t N_new = N + 1;
+                const float s_new = s + C_new;
+                if (!(((ok_mask >> j) & 1ull) && s_new <= B && N_new <= M)) {
+                    stop = j;
+                    break;
+                }
+                C = C_new;
+                N = N_new;
             }
         }
+        if (stop >= 0) {                              // first infeasible position
+            a = (int32_t)(c0 + stop);
+            next = (int32_t)lane_u32(y, stop);         // recovery token y*_{a+1}
+            done = true;
+        } else if (K - c0 < 64) {                     // the bonus row is in this chunk
+            a = K;
+            next = (int32_t)lane_u32(y, (int)(K - c0));
+            done = true;
+        }
+    }
+    if (lane == 0) {
+        if (N > 0) A.budget[i].y = s + C;             // s' = s + C_a
+        A.out_accept_len[i] = a;
+        A.out_next_token[i] = next;
     }
 }
 
@@ -496,30 +537,45 @@ hipError_t launch_verify(const Plan& plan, const CallArgs& a, void* workspace,
     unsigned char* ws = (unsigned char*)workspace;
     RowRecord* records = (RowRecord*)(ws + plan.off_records);
     TilePartial* partials = plan.splits > 1 ? (TilePartial*)(ws + plan.off_partials) : nullptr;
-    int32_t* counters = plan.splits > 1 ? (int32_t*)(ws + plan.off_counters) : nullptr;
+    int64_t* packed = a.row_offsets ? nullptr : (int64_t*)(ws + plan.off_offsets);
 
     const dim3 grid((unsigned)(plan.rows * plan.splits));
+    int32_t* row_argmax = plan.splits == 1 ? a.out_argmax : nullptr;
     if (plan.elem_bytes == 2)
         asd_row_kernel<2><<<grid, kRowThreads, 0, stream>>>(
             (const unsigned char*)a.logits, plan.vocab, plan.splits, plan.chunk_vecs,
-            a.draft_tokens, partials, counters, records, a.out_argmax, a.out_regret);
+            a.draft_tokens, partials, records, row_argmax, a.num_requests, a.block_lens, packed);
     else
         asd_row_kernel<4><<<grid, kRowThreads, 0, stream>>>(
             (const unsigned char*)a.logits, plan.vocab, plan.splits, plan.chunk_vecs,
-            a.draft_tokens, partials, counters, records, a.out_argmax, a.out_regret);
+            a.draft_tokens, partials, records, row_argmax, a.num_requests, a.block_lens, packed);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
 
-    if (a.row_offsets) {
-        const unsigned blocks = (unsigned)((a.num_requests + kScanThreads - 1) / kScanThreads);
-        asd_scan_offsets_kernel<<<blocks, kScanThreads, 0, stream>>>(
-            a.num_requests, plan.rows, a.block_lens, a.row_offsets, a.tau, a.exc_cap, a.budget,
-            records, a.out_accept_len, a.out_next_token, a.out_regret);
-    } else {
-        asd_scan_packed_kernel<<<1, kScanThreads, 0, stream>>>(
-            a.num_requests, plan.rows, a.block_lens, a.tau, a.exc_cap, a.budget, records,
-            a.out_accept_len, a.out_next_token, a.out_regret);
-    }
+    ScanArgs A;
+    A.num_requests = a.num_requests;
+    A.request_blocks = (int32_t)((a.num_requests + kScanThreads / 64 - 1) / (kScanThreads / 64));
+    A.total_rows = plan.rows;
+    A.vocab = plan.vocab;
+    A.elem_bytes = plan.elem_bytes;
+    A.splits = plan.splits;
+    A.chunk_vecs = plan.chunk_vecs;
+    A.logits = (const unsigned char*)a.logits;
+    A.draft_tokens = a.draft_tokens;
+    A.block_lens = a.block_lens;
+    A.offsets = a.row_offsets ? a.row_offsets : packed;
+    A.tau = a.tau;
+    A.exc_cap = a.exc_cap;
+    A.budget = a.budget;
+    A.records = records;
+    A.partials = partials;
+    A.out_accept_len = a.out_accept_len;
+    A.out_next_token = a.out_next_token;
+    A.out_regret = a.out_regret;
+    A.out_argmax = a.out_argmax;
+    const int64_t row_blocks =
+        (plan.splits > 1 && a.out_argmax) ? (plan.rows + kScanThreads - 1) / kScanThreads : 0;
+    asd_scan_kernel<<<(unsigned)(A.request_blocks + row_blocks), kScanThreads, 0, stream>>>(A);
     return hipGetLastError();
 }
 

@@ -14,15 +14,11 @@ constexpr int kRowThreads = 256;
 constexpr int kScanThreads = 256;
 // Largest number of vocabulary splits of one row.
 constexpr int kMaxSplits = 64;
-// Per-row completion counters live in a fixed region at the start of every
-// workspace, whatever the call's shape, so that no other shape's data ever
-// lands on them.  Rows are split over several workgroups only when there are
-// at most this many rows.
-constexpr int kCounterSlots = 4096;
 
-// One tile's best candidate: (key, column) packed so that a larger value means
-// a greater logit, and among equal logits a lower column; plus the logit's
-// binary32 bit pattern and the gathered draft logit when the tile owns it.
+// One tile's best candidate when a row is split over several workgroups:
+// (key, column) packed so that a larger value means a greater logit and, among
+// equal logits, a lower column; the logit's binary32 bit pattern; and, in the
+// tile that owns the draft token's column, that column's logit.
 struct alignas(16) TilePartial {
     unsigned long long packed;
     uint32_t bits;
@@ -45,14 +41,14 @@ struct Plan {
     int elem_bytes;          // 2 (bf16) or 4 (f32)
     int64_t vocab;
     int64_t rows;
+    int32_t num_requests;
     int splits;              // S >= 1 vocabulary splits per row
     int64_t chunk_vecs;      // 16-byte vectors per split (multiple of kRowThreads)
-    // Workspace layout (byte offsets from the workspace base; 256-byte aligned):
-    // [0, kCounterSlots * 4) completion counters, zero between calls;
-    // then the row records; then the split partials (splits > 1 only).
-    size_t off_counters;
-    size_t off_records;
-    size_t off_partials;
+    // Workspace layout (byte offsets from the workspace base; 256-byte aligned).
+    // Nothing in it is carried from one call to the next.
+    size_t off_offsets;      // int64 [num_requests]: packed row offsets
+    size_t off_records;      // RowRecord [rows] (splits == 1)
+    size_t off_partials;     // TilePartial [rows * splits] (splits > 1)
     size_t ws_bytes;
 };
 
@@ -72,7 +68,8 @@ struct CallArgs {
     float* out_regret;
 };
 
-Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int num_cus);
+Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int32_t num_requests,
+               int num_cus);
 
 hipError_t launch_verify(const Plan& plan, const CallArgs& args, void* workspace,
                          hipStream_t stream);

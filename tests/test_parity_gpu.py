@@ -248,14 +248,15 @@ def test_caller_workspace_matches_library_workspace():
     nbytes = asd.asd_workspace_bytes(torch.bfloat16, w.vocab, w.num_requests,
                                      w.logits.shape[0])
     assert nbytes > 0
-    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda:0")
+    # Any content will do: nothing in the workspace is carried between calls.
+    ws = torch.full((nbytes,), 0xA5, dtype=torch.uint8, device="cuda:0")
     a = gpu_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget,
                    workspace=ws)
     b = gpu_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget,
-                   workspace=ws)              # reused: counters were left at zero
+                   workspace=ws)
     r = oracle_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
     assert not mismatches(a, r) and not mismatches(b, r)
-    small = torch.zeros(max(nbytes - 256, 256), dtype=torch.uint8, device="cuda:0")
+    small = torch.zeros(nbytes - 256, dtype=torch.uint8, device="cuda:0")
     with pytest.raises(asd.AsdError):
         gpu_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget,
                    workspace=small)
@@ -306,3 +307,23 @@ def test_alternating_shapes_share_one_workspace():
         draft = np.where(rng.random(rows) < 0.7, y, rng.integers(0, vocab, rows)).astype(np.int32)
         check(logits, draft, [rows - 1], 2.0, 2, [[5.0, 0.0]],
               label="alternate-%d-%d-%s" % (rows, vocab, dtype))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_without_optional_per_row_outputs(cfg):
+    """The serving path: no out_argmax / out_regret (split and unsplit plans)."""
+    import paper_2608_03447_amd as asd
+    w = W.make_config(cfg, batch=None if cfg != 3 else 40)
+    lg, dr = w.call(0)
+    dev = torch.device("cuda:0")
+    from asd_gpu import device_logits
+    budget = torch.from_numpy(w.budget.copy()).to(dev)
+    acc, nxt = asd.asd_verify(device_logits(lg, dev), torch.from_numpy(dr).to(dev),
+                              torch.from_numpy(w.block_lens).to(dev),
+                              torch.from_numpy(w.tau).to(dev),
+                              torch.from_numpy(w.exc_cap).to(dev), budget)
+    torch.cuda.synchronize()
+    r = oracle_verify(lg, dr, w.block_lens, w.tau, w.exc_cap, w.budget)
+    assert np.array_equal(acc.cpu().numpy(), r["accept_len"])
+    assert np.array_equal(nxt.cpu().numpy(), r["next_token"])
+    assert np.array_equal(budget.cpu().numpy().view(np.uint32), r["budget"].view(np.uint32))
