@@ -78,15 +78,33 @@ template <> struct KeyTraits<4> {
     static constexpr int32_t kNone = (int32_t)0x80000000;   // f32 keys >= -0x7fffffff
 };
 
-// Max key over the 16-byte vectors of one group (per-dtype).
-template <int EB, bool kMasked>
+// Two ways to rank the logits of a tile.
+//  kRaw = false: the exact keys above.
+//  kRaw = true:  the raw bit patterns read as signed integers.  For every
+//                pattern with the sign bit clear (+0 aside) this equals the
+//                exact key, and every pattern with the sign bit set reads as
+//                negative.  So when the tile holds any pattern >= 1 (a positive
+//                value or positive NaN), the raw maximum is the exact maximum,
+//                found with one integer max per element instead of four ops.
+//                Tiles without one are ranked again with exact keys.
+constexpr int32_t kRawExactFrom = 1;
+
+template <int EB, bool kRaw>
+__device__ __forceinline__ uint32_t dword_keys(uint32_t w) {
+    if constexpr (kRaw) return w;
+    else if constexpr (EB == 2) return bf16x2_keys(w);
+    else return (uint32_t)f32_key(w);
+}
+
+// Max key over the 16-byte vectors of one group; vectors u >= nvalid are ignored.
+template <int EB, bool kRaw, bool kMasked>
 __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], int nvalid) {
     if constexpr (EB == 2) {
         uint32_t acc = KeyTraits<2>::kNonePacked;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            uint32_t k0 = bf16x2_keys(raw[u].x), k1 = bf16x2_keys(raw[u].y);
-            uint32_t k2 = bf16x2_keys(raw[u].z), k3 = bf16x2_keys(raw[u].w);
+            const uint32_t k0 = dword_keys<2, kRaw>(raw[u].x), k1 = dword_keys<2, kRaw>(raw[u].y);
+            const uint32_t k2 = dword_keys<2, kRaw>(raw[u].z), k3 = dword_keys<2, kRaw>(raw[u].w);
             uint32_t m = pkmax16(pkmax16(k0, k1), pkmax16(k2, k3));
             if (kMasked && u >= nvalid) m = KeyTraits<2>::kNonePacked;
             acc = pkmax16(acc, m);
@@ -98,8 +116,10 @@ __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], in
         int32_t acc = KeyTraits<4>::kNone;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            int32_t m = max(max(f32_key(raw[u].x), f32_key(raw[u].y)),
-                            max(f32_key(raw[u].z), f32_key(raw[u].w)));
+            int32_t m = max(max((int32_t)dword_keys<4, kRaw>(raw[u].x),
+                                (int32_t)dword_keys<4, kRaw>(raw[u].y)),
+                            max((int32_t)dword_keys<4, kRaw>(raw[u].z),
+                                (int32_t)dword_keys<4, kRaw>(raw[u].w)));
             if (kMasked && u >= nvalid) m = KeyTraits<4>::kNone;
             acc = max(acc, m);
         }
@@ -107,29 +127,36 @@ __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], in
     }
 }
 
+// Key of a bf16 bit pattern (low 16 bits of h16) or f32 bit pattern.
+template <int EB, bool kRaw>
+__device__ __forceinline__ int32_t key_of(uint32_t pattern) {
+    if constexpr (EB == 2) return kRaw ? (int32_t)(int16_t)pattern : bf16_key(pattern);
+    else return kRaw ? (int32_t)pattern : f32_key(pattern);
+}
+
 // Element e of a 16-byte vector as (key, binary32 bits).
-template <int EB>
+template <int EB, bool kRaw>
 __device__ __forceinline__ void element_of(const u32x4& v, int e, int32_t& key, uint32_t& bits) {
     if constexpr (EB == 2) {
         const uint32_t w = v[e >> 1];
         const uint32_t h = (e & 1) ? (w >> 16) : (w & 0xffffu);
-        key = bf16_key(h);
+        key = key_of<2, kRaw>(h);
         bits = h << 16;
     } else {
         bits = v[e];
-        key = f32_key(bits);
+        key = key_of<4, kRaw>(bits);
     }
 }
 
-template <int EB>
+template <int EB, bool kRaw>
 __device__ __forceinline__ void load_scalar(const unsigned char* p, int32_t& key, uint32_t& bits) {
     if constexpr (EB == 2) {
         const uint32_t h = *(const unsigned short*)p;
-        key = bf16_key(h);
+        key = key_of<2, kRaw>(h);
         bits = h << 16;
     } else {
         bits = *(const uint32_t*)p;
-        key = f32_key(bits);
+        key = key_of<4, kRaw>(bits);
     }
 }
 
@@ -141,6 +168,9 @@ __device__ __forceinline__ unsigned long long pack_kc(int32_t key, int64_t col) 
 }
 __device__ __forceinline__ int32_t packed_col(unsigned long long p) {
     return (int32_t)(0xffffffffu - (uint32_t)(p & 0xffffffffull));
+}
+__device__ __forceinline__ int32_t packed_key(unsigned long long p) {
+    return (int32_t)((uint32_t)(p >> 32) ^ 0x80000000u);
 }
 
 __device__ __forceinline__ void take_better(unsigned long long& p, uint32_t& bits,
@@ -230,6 +260,105 @@ __device__ void write_packed_offsets(int32_t num_requests, const int32_t* __rest
     }
 }
 
+// One lane's best (key, column) and bits over its share of a tile: the
+// tile's 16-byte vectors [split * chunk_vecs, ...) of the row's aligned middle,
+// plus the row's unaligned head (split 0) and tail (last split) elements.
+template <int EB, bool kRaw>
+__device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const RowGeom& geom,
+                                          int64_t vocab, int split, int splits,
+                                          int64_t chunk_vecs, int tid,
+                                          unsigned long long& packed, uint32_t& bits) {
+    constexpr int kEpv = 16 / EB;
+    // stream this tile's 16-byte vectors
+    const u32x4* vec = (const u32x4*)(row_ptr + geom.head * EB);
+    const int64_t v0 = (int64_t)split * chunk_vecs;
+    const int64_t v1 = min(v0 + chunk_vecs, geom.nvec);
+    const int64_t nv = v1 > v0 ? v1 - v0 : 0;
+    const int64_t nfull = nv / kGroupVecs;
+
+    int32_t best_key = kRaw ? KeyTraits<4>::kNone : KeyTraits<EB>::kNone;
+    int64_t best_group = -1;
+    int best_nvalid = 0;
+    u32x4 saved[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) saved[u] = (u32x4)(0u);
+
+    for (int64_t g = 0; g < nfull; ++g) {
+        const u32x4* p = vec + v0 + g * kGroupVecs + tid;
+        u32x4 raw[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) raw[u] = __builtin_nontemporal_load(p + u * kRowThreads);
+        const int32_t gk = group_max_key<EB, kRaw, false>(raw, kUnroll);
+        const bool better = gk > best_key;
+        best_key = better ? gk : best_key;
+        best_group = better ? g : best_group;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) saved[u] = better ? raw[u] : saved[u];
+    }
+    best_nvalid = best_group >= 0 ? kUnroll : 0;
+
+    if (nv > nfull * kGroupVecs) {       // the tile's last, partial group
+        const int64_t g = nfull;
+        const int64_t first = v0 + g * kGroupVecs + tid;
+        int nvalid = 0;
+        u32x4 raw[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            raw[u] = (u32x4)(0u);
+            if (first + u * kRowThreads < v1) {
+                raw[u] = __builtin_nontemporal_load(vec + first + u * kRowThreads);
+                ++nvalid;
+            }
+        }
+        const int32_t gk = group_max_key<EB, kRaw, true>(raw, nvalid);
+        if (nvalid > 0 && gk > best_key) {
+            best_key = gk;
+            best_group = g;
+            best_nvalid = nvalid;
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) saved[u] = raw[u];
+        }
+    }
+
+    // this lane's first element holding best_key
+    packed = pack_kc(KeyTraits<4>::kNone, 0x7fffffff);
+    bits = 0;
+    if (best_group >= 0) {
+        bool found = false;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+#pragma unroll
+            for (int e = 0; e < kEpv; ++e) {
+                int32_t k;
+                uint32_t b;
+                element_of<EB, kRaw>(saved[u], e, k, b);
+                if (!found && u < best_nvalid && k == best_key) {
+                    found = true;
+                    const int64_t vi = v0 + best_group * kGroupVecs + u * kRowThreads + tid;
+                    packed = pack_kc(k, geom.head + vi * kEpv + e);
+                    bits = b;
+                }
+            }
+        }
+    }
+
+    // unaligned head and tail elements (at most 16 / EB - 1 of each)
+    if (split == 0 && tid < geom.head) {
+        int32_t k;
+        uint32_t b;
+        load_scalar<EB, kRaw>(row_ptr + (int64_t)tid * EB, k, b);
+        take_better(packed, bits, pack_kc(k, tid), b);
+    }
+    if (split == splits - 1 && tid < vocab - geom.tail) {
+        const int64_t c = geom.tail + tid;
+        int32_t k;
+        uint32_t b;
+        load_scalar<EB, kRaw>(row_ptr + c * EB, k, b);
+        take_better(packed, bits, pack_kc(k, c), b);
+    }
+
+}
+
 // ----------------------------------------------------------- stage 1 kernel
 
 template <int EB>
@@ -257,98 +386,22 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
     uint32_t draft_bits = 0;
     if (owns_x && tid == 0) {
         int32_t k_unused;
-        load_scalar<EB>(row_ptr + (int64_t)x * EB, k_unused, draft_bits);
+        load_scalar<EB, true>(row_ptr + (int64_t)x * EB, k_unused, draft_bits);
     }
 
-    // ---- stream this tile's 16-byte vectors
-    const u32x4* vec = (const u32x4*)(row_ptr + geom.head * EB);
-    const int64_t v0 = (int64_t)split * chunk_vecs;
-    const int64_t v1 = min(v0 + chunk_vecs, geom.nvec);
-    const int64_t nv = v1 > v0 ? v1 - v0 : 0;
-    const int64_t nfull = nv / kGroupVecs;
-
-    int32_t best_key = KeyTraits<EB>::kNone;
-    int64_t best_group = -1;
-    int best_nvalid = 0;
-    u32x4 saved[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) saved[u] = (u32x4)(0u);
-
-    for (int64_t g = 0; g < nfull; ++g) {
-        const u32x4* p = vec + v0 + g * kGroupVecs + tid;
-        u32x4 raw[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) raw[u] = __builtin_nontemporal_load(p + u * kRowThreads);
-        const int32_t gk = group_max_key<EB, false>(raw, kUnroll);
-        const bool better = gk > best_key;
-        best_key = better ? gk : best_key;
-        best_group = better ? g : best_group;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) saved[u] = better ? raw[u] : saved[u];
-    }
-    best_nvalid = best_group >= 0 ? kUnroll : 0;
-
-    if (nv > nfull * kGroupVecs) {       // the tile's last, partial group
-        const int64_t g = nfull;
-        const int64_t first = v0 + g * kGroupVecs + tid;
-        int nvalid = 0;
-        u32x4 raw[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            raw[u] = (u32x4)(0u);
-            if (first + u * kRowThreads < v1) {
-                raw[u] = __builtin_nontemporal_load(vec + first + u * kRowThreads);
-                ++nvalid;
-            }
-        }
-        const int32_t gk = group_max_key<EB, true>(raw, nvalid);
-        if (gk > best_key) {
-            best_key = gk;
-            best_group = g;
-            best_nvalid = nvalid;
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) saved[u] = raw[u];
-        }
-    }
-
-    // ---- this lane's first element holding best_key
-    unsigned long long packed = pack_kc(KeyTraits<4>::kNone, 0x7fffffff);
-    uint32_t bits = 0;
-    if (best_group >= 0) {
-        bool found = false;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-#pragma unroll
-            for (int e = 0; e < kEpv; ++e) {
-                int32_t k;
-                uint32_t b;
-                element_of<EB>(saved[u], e, k, b);
-                if (!found && u < best_nvalid && k == best_key) {
-                    found = true;
-                    const int64_t vi = v0 + best_group * kGroupVecs + u * kRowThreads + tid;
-                    packed = pack_kc(k, geom.head + vi * kEpv + e);
-                    bits = b;
-                }
-            }
-        }
-    }
-
-    // ---- unaligned head and tail elements (at most 16 / EB - 1 of each)
-    if (split == 0 && tid < geom.head) {
-        int32_t k;
-        uint32_t b;
-        load_scalar<EB>(row_ptr + (int64_t)tid * EB, k, b);
-        take_better(packed, bits, pack_kc(k, tid), b);
-    }
-    if (split == splits - 1 && tid < vocab - geom.tail) {
-        const int64_t c = geom.tail + tid;
-        int32_t k;
-        uint32_t b;
-        load_scalar<EB>(row_ptr + c * EB, k, b);
-        take_better(packed, bits, pack_kc(k, c), b);
-    }
-
+    // ---- rank the tile by raw patterns; if it holds no positive pattern the
+    // raw order is not the exact one, so rank it again with exact keys.
+    unsigned long long packed;
+    uint32_t bits;
+    tile_best<EB, true>(row_ptr, geom, vocab, split, splits, chunk_vecs, tid, packed, bits);
     block_reduce(packed, bits);
+    __shared__ int s_exact;
+    if (tid == 0) s_exact = packed_key(packed) < kRawExactFrom;
+    __syncthreads();
+    if (s_exact) {
+        tile_best<EB, false>(row_ptr, geom, vocab, split, splits, chunk_vecs, tid, packed, bits);
+        block_reduce(packed, bits);
+    }
     if (tid != 0) return;
 
     if (splits > 1) {                    // combined by the scan kernel
