@@ -465,10 +465,19 @@ __device__ __forceinline__ void combine_row(const ScanArgs& A, int64_t row, int3
     packed = 0;
     bits = 0;
     draft_bits = 0;
-    for (int s = 0; s < A.splits; ++s) {
-        const TilePartial tp = parts[s];
-        take_better(packed, bits, tp.packed, tp.bits);
-        if (s == owner) draft_bits = tp.draft_bits;
+    // Partials are read eight at a time so that their loads are in flight together.
+    for (int s0 = 0; s0 < A.splits; s0 += 8) {
+        TilePartial tp[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (s0 + j < A.splits) tp[j] = parts[s0 + j];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (s0 + j < A.splits) {
+                take_better(packed, bits, tp[j].packed, tp[j].bits);
+                if (s0 + j == owner) draft_bits = tp[j].draft_bits;
+            }
+        }
     }
 }
 
