@@ -12,6 +12,9 @@ Prints one JSON line on stdout; progress goes to stderr.
 
 Workload 1 is one request decoding 64 sequential blocks: a step is then the
 64 calls, with the ledger carried in device memory from call to call.
+With --shards N every row is split into N column shards in separate buffers
+(the layout N tensor-parallel ranks hold), and a step is N shard passes plus
+the verification from their partials, all on this one GPU.
     python bench.py --copy-calibration     # plain copy of known size, for
                                            # scaling rocprofv3 FETCH/WRITE_SIZE
 """
@@ -98,6 +101,10 @@ def main():
                     help="bound on the CPU-oracle baseline's timed work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--shards", type=int, default=0,
+                    help="vocabulary-sharded verification: split every row into this many "
+                         "column shards held in separate buffers (as tensor-parallel ranks hold "
+                         "them), reduce each with asd_shard_argmax, then asd_verify_partials")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -141,6 +148,22 @@ def main():
         for lg, dr, a, x in calls:
             asd.asd_verify(lg, dr, lens, tau, cap, budget, out_accept_len=a, out_next_token=x)
 
+    if args.shards > 0:
+        if w.blocks != 1:
+            raise SystemExit("--shards needs a single-call workload (2..5)")
+        width = -(-w.vocab // args.shards)
+        shard_bufs = [logits[:, k * width:min((k + 1) * width, w.vocab)].contiguous()
+                      for k in range(args.shards)]
+        parts = torch.empty((args.shards, w.rows_per_call, 4), dtype=torch.int32, device=dev)
+        del logits, calls
+        torch.cuda.synchronize()
+
+        def step():
+            for k, sb in enumerate(shard_bufs):
+                asd.asd_shard_argmax(sb, k * width, w.vocab, draft, out_partials=parts[k])
+            asd.asd_verify_partials(parts, width, w.vocab, draft, lens, tau, cap, budget,
+                                    out_accept_len=acc[0], out_next_token=nxt[0])
+
     # Parity step on the pristine ledger (checked against the oracle below).
     step()
     torch.cuda.synchronize()
@@ -177,14 +200,16 @@ def main():
     # Context: torch's own full reduction over the same logits (a read-only pass).
     pe0 = torch.cuda.Event(enable_timing=True)
     pe1 = torch.cuda.Event(enable_timing=True)
-    for _ in range(3):
-        torch.amax(logits)
-    pe0.record(stream)
-    for _ in range(10):
-        torch.amax(logits)
-    pe1.record(stream)
-    torch.cuda.synchronize()
-    probe_gbps = w.logit_bytes_per_call * 10 / (pe0.elapsed_time(pe1) / 1e3) / 1e9
+    probe_gbps = None
+    if args.shards == 0:
+        for _ in range(3):
+            torch.amax(logits)
+        pe0.record(stream)
+        for _ in range(10):
+            torch.amax(logits)
+        pe1.record(stream)
+        torch.cuda.synchronize()
+        probe_gbps = w.logit_bytes_per_call * 10 / (pe0.elapsed_time(pe1) / 1e3) / 1e9
 
     # Oracle: parity reference and CPU baseline (single-threaded, as written).
     parity = "not checked"
@@ -226,9 +251,12 @@ def main():
     tag = "b%d_k%s_v%d_%s" % (w.num_requests, kdesc, w.vocab, w.dtype)
     if w.blocks > 1:
         tag += "_seq%d" % w.blocks
+    if args.shards > 0:
+        tag += "_shards%d" % args.shards
     traffic = read_traffic(tag, kernel_source_hash())
-    metric = METRIC if args.config == 3 else (
-        "verified logit rows/s + achieved HBM GB/s (%s)" % w.name)
+    metric = METRIC if (args.config == 3 and not args.shards) else (
+        "verified logit rows/s + achieved HBM GB/s (%s%s)" % (
+            w.name, ", %d vocabulary shards" % args.shards if args.shards else ""))
     out = {
         "metric": metric,
         "value": rows_per_s,
@@ -247,8 +275,12 @@ def main():
                                "tau/cap/budgets per request%s" % (
                                    w.name, w.num_requests, kdesc.replace("to", ".."),
                                    w.vocab, w.dtype,
-                                   ", %d sequential calls per step" % w.blocks
-                                   if w.blocks > 1 else ""),
+                                   (", %d sequential calls per step" % w.blocks
+                                    if w.blocks > 1 else "") +
+                                   (", vocabulary split into %d column shards (asd_shard_argmax"
+                                    " x %d + asd_verify_partials) on one GPU"
+                                    % (args.shards, args.shards) if args.shards else "")),
+                   "vocab_shards": args.shards or 1,
                    "calls_per_step": w.blocks,
                    "rows_per_call": w.rows_per_call, "vocab": w.vocab,
                    "num_requests": w.num_requests,

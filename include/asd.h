@@ -141,6 +141,63 @@ asd_status asd_verify_ws(const void *logits, asd_dtype dtype, int64_t vocab,
                          int32_t *out_argmax, float *out_regret, void *stream,
                          void *workspace, size_t workspace_bytes);
 
+/*
+ * Vocabulary-sharded (tensor-parallel) verification.  The verifier needs, per
+ * row, only the greatest logit, its column and the draft token's logit
+ * (Sec. 3.3), so each holder of a column shard can reduce its own columns and
+ * only 16 bytes per row need to meet: no K x |V| logit buffer is gathered.
+ */
+
+/* One shard's result for one row (16 bytes, 16-byte aligned; contents opaque). */
+typedef struct {
+    uint32_t opaque[4];
+} asd_row_partial;
+
+/*
+ * asd_shard_argmax -- the row pass of asd_verify (Eqs. 1 and 3) on one shard.
+ *
+ * shard_logits    [total_rows, shard_vocab], row-major, dense, dtype elements:
+ *                 row r holds columns [vocab_offset, vocab_offset + shard_vocab)
+ *                 of the full vocabulary of row r.  Base address a multiple of
+ *                 the element size.
+ * vocab           V, the full vocabulary size: vocab_offset >= 0,
+ *                 shard_vocab >= 1, vocab_offset + shard_vocab <= V < 2^30.
+ * total_rows      rows, 1 <= total_rows < 2^31.
+ * draft_tokens    int32 [total_rows], global token ids as for asd_verify.
+ * out_partials    asd_row_partial [total_rows]: the shard's greatest value and
+ *                 its global column (argmax order of asd_verify), and the draft
+ *                 token's logit when its id lies in the shard.
+ * Allocates nothing and uses no workspace.  Asynchronous on `stream`.
+ */
+asd_status asd_shard_argmax(const void *shard_logits, asd_dtype dtype, int64_t shard_vocab,
+                            int64_t vocab_offset, int64_t vocab, int64_t total_rows,
+                            const int32_t *draft_tokens, asd_row_partial *out_partials,
+                            void *stream);
+
+/*
+ * asd_verify_partials -- finish asd_verify from the partials of all shards.
+ *
+ * partials        asd_row_partial [num_shards][total_rows] (shard-major), shard k
+ *                 written by asd_shard_argmax for columns
+ *                 [k * shard_vocab, min((k + 1) * shard_vocab, V)).  With one
+ *                 shard per GPU they are gathered to one device first.
+ * num_shards      1 <= num_shards <= 4096, and the shards cover V exactly:
+ *                 (num_shards - 1) * shard_vocab < V <= num_shards * shard_vocab.
+ * The other arguments and every output are those of asd_verify, and the results
+ * are bit-identical to asd_verify on the unsharded rows.  When row_offsets is
+ * NULL and num_requests > 1024 the packed offsets are computed into the
+ * library workspace of this (device, stream) pair (allocated on first use, see
+ * asd_verify); otherwise nothing is allocated.
+ */
+asd_status asd_verify_partials(const asd_row_partial *partials, int32_t num_shards,
+                               int64_t shard_vocab, int64_t vocab, int32_t num_requests,
+                               int64_t total_rows, const int32_t *draft_tokens,
+                               const int32_t *block_lens, const int64_t *row_offsets,
+                               const float *tau, const int32_t *exc_cap,
+                               asd_budget *budget_inout, int32_t *out_accept_len,
+                               int32_t *out_next_token, int32_t *out_argmax,
+                               float *out_regret, void *stream);
+
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 

@@ -13,8 +13,9 @@ import torch
 
 from .build import LIBRARY
 
-__all__ = ["asd_verify", "asd_verify_ws", "asd_workspace_bytes", "asd_status_string",
-           "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16", "library_path"]
+__all__ = ["asd_verify", "asd_verify_ws", "asd_shard_argmax", "asd_verify_partials",
+           "asd_workspace_bytes", "asd_status_string", "asd_version", "asd_release", "AsdError",
+           "ASD_F32", "ASD_BF16", "library_path"]
 
 ASD_F32 = 0
 ASD_BF16 = 1
@@ -47,6 +48,11 @@ def _load():
     lib.asd_verify.restype = ctypes.c_int
     lib.asd_verify_ws.argtypes = common + [vp, sz]
     lib.asd_verify_ws.restype = ctypes.c_int
+    lib.asd_shard_argmax.argtypes = [vp, ctypes.c_int, i64, i64, i64, i64, vp, vp, vp]
+    lib.asd_shard_argmax.restype = ctypes.c_int
+    lib.asd_verify_partials.argtypes = [vp, i32, i64, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp,
+                                         vp, vp, vp, vp]
+    lib.asd_verify_partials.restype = ctypes.c_int
     lib.asd_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i64]
     lib.asd_workspace_bytes.restype = sz
     lib.asd_status_string.argtypes = [ctypes.c_int]
@@ -86,14 +92,18 @@ def _per_request(value, n, dtype, device, name):
     return torch.full((n,), value, dtype=dtype, device=device)
 
 
-def _marshal(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets,
-             out_accept_len, out_next_token, out_argmax, out_regret):
+def _check_logits(logits):
     if logits.dim() != 2 or logits.dtype not in _DTYPES or not logits.is_cuda:
         raise ValueError("logits must be a 2-D float32 or bfloat16 tensor on a GPU")
     if not logits.is_contiguous():
         raise ValueError("logits must be contiguous (row-major, dense)")
-    dev = logits.device
-    rows, vocab = logits.shape
+
+
+def _marshal(dev, rows, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets,
+             out_accept_len, out_next_token, out_argmax, out_regret):
+    """Checks and pointers of the arguments shared by every verifying call:
+    [num_requests, total_rows, draft, lens, offsets, tau, cap, budget, accept,
+    next, argmax, regret, stream]."""
     if block_lens.dtype != torch.int32 or block_lens.dim() != 1 or block_lens.device != dev:
         raise ValueError("block_lens must be an int32 vector on the logits' device")
     n = block_lens.shape[0]
@@ -126,9 +136,9 @@ def _marshal(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets
         return None if t is None else ctypes.c_void_p(t.data_ptr())
 
     stream = torch.cuda.current_stream(dev).cuda_stream
-    args = [p(logits), _DTYPES[logits.dtype], vocab, n, rows, p(draft_tokens), p(block_lens),
-            p(row_offsets), p(tau), p(exc_cap), p(budget), p(out_accept_len), p(out_next_token),
-            p(out_argmax), p(out_regret), ctypes.c_void_p(stream)]
+    args = [n, rows, p(draft_tokens), p(block_lens), p(row_offsets), p(tau), p(exc_cap),
+            p(budget), p(out_accept_len), p(out_next_token), p(out_argmax), p(out_regret),
+            ctypes.c_void_p(stream)]
     keep = (tau, exc_cap, block_lens, draft_tokens)
     return args, out_accept_len, out_next_token, keep
 
@@ -146,11 +156,13 @@ def asd_verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, *, row_of
     Returns ``(accept_len, next_token)`` int32 tensors; the work is enqueued on
     the current stream of the logits' device.
     """
+    _check_logits(logits)
     with torch.cuda.device(logits.device):
-        args, acc, nxt, keep = _marshal(logits, draft_tokens, block_lens, tau, exc_cap, budget,
-                                        row_offsets, out_accept_len, out_next_token,
-                                        out_argmax, out_regret)
-        st = _load().asd_verify(*args)
+        args, acc, nxt, keep = _marshal(logits.device, logits.shape[0], draft_tokens, block_lens,
+                                        tau, exc_cap, budget, row_offsets, out_accept_len,
+                                        out_next_token, out_argmax, out_regret)
+        st = _load().asd_verify(ctypes.c_void_p(logits.data_ptr()), _DTYPES[logits.dtype],
+                                logits.shape[1], *args)
     del keep
     if st != 0:
         raise AsdError(st, "asd_verify")
@@ -163,13 +175,77 @@ def asd_verify_ws(logits, draft_tokens, block_lens, tau, exc_cap, budget, worksp
     """``asd_verify`` with a caller-provided workspace (a zero-initialised uint8 tensor)."""
     if workspace.dtype != torch.uint8 or not workspace.is_contiguous():
         raise ValueError("workspace must be a contiguous uint8 tensor")
+    _check_logits(logits)
     with torch.cuda.device(logits.device):
-        args, acc, nxt, keep = _marshal(logits, draft_tokens, block_lens, tau, exc_cap, budget,
-                                        row_offsets, out_accept_len, out_next_token,
-                                        out_argmax, out_regret)
-        st = _load().asd_verify_ws(*args, ctypes.c_void_p(workspace.data_ptr()),
-                                   workspace.numel())
+        args, acc, nxt, keep = _marshal(logits.device, logits.shape[0], draft_tokens, block_lens,
+                                        tau, exc_cap, budget, row_offsets, out_accept_len,
+                                        out_next_token, out_argmax, out_regret)
+        st = _load().asd_verify_ws(ctypes.c_void_p(logits.data_ptr()), _DTYPES[logits.dtype],
+                                   logits.shape[1], *args,
+                                   ctypes.c_void_p(workspace.data_ptr()), workspace.numel())
     del keep
     if st != 0:
         raise AsdError(st, "asd_verify_ws")
+    return acc, nxt
+
+
+def asd_shard_argmax(shard_logits, vocab_offset, vocab, draft_tokens, out_partials=None):
+    """Row pass of one vocabulary shard (``asd_shard_argmax`` of ``include/asd.h``).
+
+    shard_logits  [total_rows, W] float32 or bfloat16: columns
+                  [vocab_offset, vocab_offset + W) of the full vocabulary
+    draft_tokens  int32 [total_rows] (global ids)
+    Returns the partials, an int32 tensor [total_rows, 4] (16 opaque bytes per row).
+    """
+    if shard_logits.dim() != 2 or shard_logits.dtype not in _DTYPES or not shard_logits.is_cuda:
+        raise ValueError("shard_logits must be a 2-D float32 or bfloat16 tensor on a GPU")
+    if not shard_logits.is_contiguous():
+        raise ValueError("shard_logits must be contiguous (row-major, dense)")
+    dev = shard_logits.device
+    rows, width = shard_logits.shape
+    if draft_tokens.dtype != torch.int32 or draft_tokens.shape != (rows,) \
+            or draft_tokens.device != dev:
+        raise ValueError("draft_tokens must be int32 of shape (%d,) on %s" % (rows, dev))
+    if out_partials is None:
+        out_partials = torch.empty((rows, 4), dtype=torch.int32, device=dev)
+    if out_partials.dtype != torch.int32 or out_partials.shape != (rows, 4) \
+            or not out_partials.is_contiguous() or out_partials.device != dev:
+        raise ValueError("out_partials must be a contiguous int32 (%d, 4) tensor on %s" % (rows, dev))
+    draft_tokens = draft_tokens.contiguous()
+    with torch.cuda.device(dev):
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        st = _load().asd_shard_argmax(ctypes.c_void_p(shard_logits.data_ptr()),
+                                      _DTYPES[shard_logits.dtype], width, int(vocab_offset),
+                                      int(vocab), rows, ctypes.c_void_p(draft_tokens.data_ptr()),
+                                      ctypes.c_void_p(out_partials.data_ptr()),
+                                      ctypes.c_void_p(stream))
+    if st != 0:
+        raise AsdError(st, "asd_shard_argmax")
+    return out_partials
+
+
+def asd_verify_partials(partials, shard_vocab, vocab, draft_tokens, block_lens, tau, exc_cap,
+                        budget, *, row_offsets=None, out_accept_len=None, out_next_token=None,
+                        out_argmax=None, out_regret=None):
+    """Finish the verification from the partials of all shards
+    (``asd_verify_partials`` of ``include/asd.h``).
+
+    partials  int32 [num_shards, total_rows, 4]; shard k holds columns
+              [k * shard_vocab, min((k + 1) * shard_vocab, vocab))
+    Other arguments as for :func:`asd_verify`.  Returns ``(accept_len, next_token)``.
+    """
+    if partials.dtype != torch.int32 or partials.dim() != 3 or partials.shape[2] != 4 \
+            or not partials.is_contiguous() or not partials.is_cuda:
+        raise ValueError("partials must be a contiguous int32 (num_shards, total_rows, 4) GPU tensor")
+    dev = partials.device
+    shards, rows = partials.shape[0], partials.shape[1]
+    with torch.cuda.device(dev):
+        args, acc, nxt, keep = _marshal(dev, rows, draft_tokens, block_lens, tau, exc_cap, budget,
+                                        row_offsets, out_accept_len, out_next_token,
+                                        out_argmax, out_regret)
+        st = _load().asd_verify_partials(ctypes.c_void_p(partials.data_ptr()), shards,
+                                         int(shard_vocab), int(vocab), *args)
+    del keep
+    if st != 0:
+        raise AsdError(st, "asd_verify_partials")
     return acc, nxt

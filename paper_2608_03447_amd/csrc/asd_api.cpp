@@ -156,6 +156,34 @@ asd_status plan_for(asd_dtype dtype, int64_t vocab, int32_t num_requests, int64_
     return ASD_OK;
 }
 
+// The library-owned workspace of (current device, stream), grown to at least
+// `bytes`; growth (hipMalloc) is refused during stream capture.
+asd_status library_workspace(hipStream_t s, size_t bytes, void** out) {
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return ASD_EHIP;
+    std::lock_guard<std::mutex> lock(g_mutex);
+    Workspace& w = g_workspaces[std::make_pair(device, s)];
+    if (w.bytes < bytes) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ASD_EHIP;
+        if (cap != hipStreamCaptureStatusNone) return ASD_ECAPTURE;
+        size_t want = bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : bytes;
+        want = align_up(want, (size_t)1 << 20);
+        if (w.ptr) {
+            if (hipStreamSynchronize(s) != hipSuccess) return ASD_EHIP;
+            (void)hipFree(w.ptr);
+            w.ptr = nullptr;
+            w.bytes = 0;
+        }
+        void* p = nullptr;
+        if (hipMalloc(&p, want) != hipSuccess) return ASD_ENOMEM;
+        w.ptr = p;
+        w.bytes = want;
+    }
+    *out = w.ptr;
+    return ASD_OK;
+}
+
 }  // namespace
 }  // namespace asd
 
@@ -177,32 +205,8 @@ asd_status asd_verify(const void* logits, asd_dtype dtype, int64_t vocab, int32_
     if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
 
     hipStream_t s = (hipStream_t)stream;
-    int device = 0;
-    if (hipGetDevice(&device) != hipSuccess) return ASD_EHIP;
     void* ws = nullptr;
-    {
-        std::lock_guard<std::mutex> lock(g_mutex);
-        Workspace& w = g_workspaces[std::make_pair(device, s)];
-        if (w.bytes < plan.ws_bytes) {
-            hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-            if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ASD_EHIP;
-            if (cap != hipStreamCaptureStatusNone) return ASD_ECAPTURE;
-            size_t want = plan.ws_bytes;
-            if (want < (size_t)1 << 20) want = (size_t)1 << 20;
-            want = align_up(want, (size_t)1 << 20);
-            if (w.ptr) {
-                if (hipStreamSynchronize(s) != hipSuccess) return ASD_EHIP;
-                (void)hipFree(w.ptr);
-                w.ptr = nullptr;
-                w.bytes = 0;
-            }
-            void* p = nullptr;
-            if (hipMalloc(&p, want) != hipSuccess) return ASD_ENOMEM;
-            w.ptr = p;
-            w.bytes = want;
-        }
-        ws = w.ptr;
-    }
+    if ((st = library_workspace(s, plan.ws_bytes, &ws)) != ASD_OK) return st;
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
                    out_argmax, out_regret, s, plan, ws);
@@ -239,6 +243,68 @@ asd_status asd_verify_ws(const void* logits, asd_dtype dtype, int64_t vocab,
                    out_argmax, out_regret, (hipStream_t)stream, plan, workspace);
 }
 
+asd_status asd_shard_argmax(const void* shard_logits, asd_dtype dtype, int64_t shard_vocab,
+                            int64_t vocab_offset, int64_t vocab, int64_t total_rows,
+                            const int32_t* draft_tokens, asd_row_partial* out_partials,
+                            void* stream) {
+    const int eb = elem_bytes_of(dtype);
+    if (eb == 0) return ASD_EDTYPE;
+    if (vocab < 1 || vocab >= ((int64_t)1 << 30) || shard_vocab < 1 || vocab_offset < 0 ||
+        vocab_offset + shard_vocab > vocab)
+        return ASD_EINVAL;
+    if (total_rows < 1 || total_rows >= ((int64_t)1 << 31)) return ASD_EINVAL;
+    if (!shard_logits || !draft_tokens || !out_partials) return ASD_EINVAL;
+    if (((uintptr_t)shard_logits % (uintptr_t)eb) != 0 || ((uintptr_t)out_partials & 15) != 0)
+        return ASD_EINVAL;
+    return launch_shard_argmax(eb, shard_logits, shard_vocab, vocab_offset, total_rows,
+                               draft_tokens, out_partials, (hipStream_t)stream) == hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
+asd_status asd_verify_partials(const asd_row_partial* partials, int32_t num_shards,
+                               int64_t shard_vocab, int64_t vocab, int32_t num_requests,
+                               int64_t total_rows, const int32_t* draft_tokens,
+                               const int32_t* block_lens, const int64_t* row_offsets,
+                               const float* tau, const int32_t* exc_cap,
+                               asd_budget* budget_inout, int32_t* out_accept_len,
+                               int32_t* out_next_token, int32_t* out_argmax, float* out_regret,
+                               void* stream) {
+    asd_status st = check_args(partials, ASD_F32, vocab, num_requests, total_rows, draft_tokens,
+                               block_lens, tau, exc_cap, budget_inout, out_accept_len,
+                               out_next_token);
+    if (st != ASD_OK || num_requests == 0) return st;
+    if (num_shards < 1 || num_shards > 4096 || shard_vocab < 1 ||
+        (int64_t)(num_shards - 1) * shard_vocab >= vocab ||
+        (int64_t)num_shards * shard_vocab < vocab)
+        return ASD_EINVAL;
+    if (((uintptr_t)partials & 15) != 0) return ASD_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = nullptr;
+    if (!row_offsets && num_requests > kWaveOffsetsMaxRequests) {
+        if ((st = library_workspace(s, align_up((size_t)num_requests * sizeof(int64_t), 256),
+                                    &ws)) != ASD_OK)
+            return st;
+    }
+    CallArgs a{};
+    a.logits = nullptr;
+    a.num_requests = num_requests;
+    a.draft_tokens = draft_tokens;
+    a.block_lens = block_lens;
+    a.row_offsets = row_offsets;
+    a.tau = tau;
+    a.exc_cap = exc_cap;
+    a.budget = reinterpret_cast<float2*>(budget_inout);
+    a.out_accept_len = out_accept_len;
+    a.out_next_token = out_next_token;
+    a.out_argmax = out_argmax;
+    a.out_regret = out_regret;
+    return launch_verify_partials(partials, num_shards, shard_vocab, vocab, total_rows, a,
+                                  (int64_t*)ws, s) == hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
 const char* asd_status_string(asd_status status) {
     switch (status) {
         case ASD_OK: return "ASD_OK";
@@ -251,7 +317,7 @@ const char* asd_status_string(asd_status status) {
     }
 }
 
-const char* asd_version(void) { return "asd-mi355x 0.1.0 gfx950"; }
+const char* asd_version(void) { return "asd-mi355x 0.2.0 gfx950"; }
 
 asd_status asd_release(void) {
     std::lock_guard<std::mutex> lock(g_mutex);

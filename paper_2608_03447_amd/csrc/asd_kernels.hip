@@ -265,8 +265,8 @@ __device__ void write_packed_offsets(int32_t num_requests, const int32_t* __rest
 // plus the row's unaligned head (split 0) and tail (last split) elements.
 template <int EB, bool kRaw>
 __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const RowGeom& geom,
-                                          int64_t vocab, int split, int splits,
-                                          int64_t chunk_vecs, int tid,
+                                          int64_t vocab, int64_t col_offset, int split,
+                                          int splits, int64_t chunk_vecs, int tid,
                                           unsigned long long& packed, uint32_t& bits) {
     constexpr int kEpv = 16 / EB;
     // stream this tile's 16-byte vectors
@@ -335,7 +335,7 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
                 if (!found && u < best_nvalid && k == best_key) {
                     found = true;
                     const int64_t vi = v0 + best_group * kGroupVecs + u * kRowThreads + tid;
-                    packed = pack_kc(k, geom.head + vi * kEpv + e);
+                    packed = pack_kc(k, col_offset + geom.head + vi * kEpv + e);
                     bits = b;
                 }
             }
@@ -347,14 +347,14 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
         int32_t k;
         uint32_t b;
         load_scalar<EB, kRaw>(row_ptr + (int64_t)tid * EB, k, b);
-        take_better(packed, bits, pack_kc(k, tid), b);
+        take_better(packed, bits, pack_kc(k, col_offset + tid), b);
     }
     if (split == splits - 1 && tid < vocab - geom.tail) {
         const int64_t c = geom.tail + tid;
         int32_t k;
         uint32_t b;
         load_scalar<EB, kRaw>(row_ptr + c * EB, k, b);
-        take_better(packed, bits, pack_kc(k, c), b);
+        take_better(packed, bits, pack_kc(k, col_offset + c), b);
     }
 
 }
@@ -362,10 +362,17 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
 // ----------------------------------------------------------- stage 1 kernel
 
 template <int EB>
+//
+// `logits` rows hold columns [col_offset, col_offset + vocab) of the full
+// vocabulary (col_offset = 0 and vocab = V unless the rows are one tensor-
+// parallel shard); columns are reported globally.  With `partials` set every
+// tile writes a partial (split rows, or one shard of each row); otherwise each
+// row is one tile and writes its record.
 __global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
-    const unsigned char* __restrict__ logits, int64_t vocab, int splits, int64_t chunk_vecs,
-    const int32_t* __restrict__ draft_tokens, TilePartial* __restrict__ partials,
-    RowRecord* __restrict__ records, int32_t* __restrict__ out_argmax, int32_t num_requests,
+    const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
+    int64_t chunk_vecs, const int32_t* __restrict__ draft_tokens,
+    TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
+    int32_t* __restrict__ out_argmax, int32_t num_requests,
     const int32_t* __restrict__ block_lens, int64_t* __restrict__ packed_offsets) {
     constexpr int kEpv = 16 / EB;
     const int tid = threadIdx.x;
@@ -381,30 +388,33 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
     // Draft token of this row (uniform); the owning tile gathers z(x) early so
     // the load overlaps the stream.
     const int32_t x = draft_tokens[row];
-    const bool x_valid = x >= 0 && (int64_t)x < vocab;
-    const bool owns_x = x_valid && owner_split(x, geom, chunk_cols, splits) == split;
+    const int64_t x_local = (int64_t)x - col_offset;
+    const bool x_here = x_local >= 0 && x_local < vocab;
+    const bool owns_x = x_here && owner_split(x_local, geom, chunk_cols, splits) == split;
     uint32_t draft_bits = 0;
     if (owns_x && tid == 0) {
         int32_t k_unused;
-        load_scalar<EB, true>(row_ptr + (int64_t)x * EB, k_unused, draft_bits);
+        load_scalar<EB, true>(row_ptr + x_local * EB, k_unused, draft_bits);
     }
 
     // ---- rank the tile by raw patterns; if it holds no positive pattern the
     // raw order is not the exact one, so rank it again with exact keys.
     unsigned long long packed;
     uint32_t bits;
-    tile_best<EB, true>(row_ptr, geom, vocab, split, splits, chunk_vecs, tid, packed, bits);
+    tile_best<EB, true>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid, packed,
+                        bits);
     block_reduce(packed, bits);
     __shared__ int s_exact;
     if (tid == 0) s_exact = packed_key(packed) < kRawExactFrom;
     __syncthreads();
     if (s_exact) {
-        tile_best<EB, false>(row_ptr, geom, vocab, split, splits, chunk_vecs, tid, packed, bits);
+        tile_best<EB, false>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
+                             packed, bits);
         block_reduce(packed, bits);
     }
     if (tid != 0) return;
 
-    if (splits > 1) {                    // combined by the scan kernel
+    if (partials != nullptr) {           // combined by the scan kernel
         TilePartial tp;
         tp.packed = packed;
         tp.bits = bits;
@@ -416,7 +426,7 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
     // ---- one tile per row: the row record (one binary32 subtraction)
     const int32_t y = packed_col(packed);
     RowRecord rec;
-    if (x_valid) {
+    if (x_here) {                        // the whole vocabulary: x_here = x in [0, V)
         rec.regret = bits_to_float(bits) - bits_to_float(draft_bits);
         rec.y_flags = (uint32_t)y | ((x != y) ? kMismatchBit : 0u);
     } else {
@@ -444,8 +454,9 @@ struct ScanArgs {
     const float* tau;
     const int32_t* exc_cap;
     float2* budget;
-    const RowRecord* records;    // splits == 1
-    const TilePartial* partials; // splits > 1
+    const RowRecord* records;    // splits == 1 and no shards
+    const TilePartial* partials; // split rows: [row][split]; shards: [shard][row]
+    int64_t shard_vocab;         // > 0: partials come from vocabulary shards of this width
     int32_t* out_accept_len;
     int32_t* out_next_token;
     float* out_regret;
@@ -456,12 +467,21 @@ struct ScanArgs {
 __device__ __forceinline__ void combine_row(const ScanArgs& A, int64_t row, int32_t x,
                                             unsigned long long& packed, uint32_t& bits,
                                             uint32_t& draft_bits) {
-    const TilePartial* parts = A.partials + row * A.splits;
-    const unsigned char* row_ptr = A.logits + row * A.vocab * A.elem_bytes;
-    const RowGeom geom = row_geom(row_ptr, A.vocab, A.elem_bytes);
-    const int owner = (x >= 0 && (int64_t)x < A.vocab)
-                          ? owner_split(x, geom, A.chunk_vecs * (16 / A.elem_bytes), A.splits)
-                          : -1;
+    const bool x_valid = x >= 0 && (int64_t)x < A.vocab;
+    const TilePartial* parts;
+    int64_t stride;
+    int owner = -1;
+    if (A.shard_vocab > 0) {             // shard k holds columns [k W, (k + 1) W)
+        parts = A.partials + row;
+        stride = A.total_rows;
+        if (x_valid) owner = (int)min((int64_t)x / A.shard_vocab, (int64_t)A.splits - 1);
+    } else {                             // tiles of one row
+        parts = A.partials + row * A.splits;
+        stride = 1;
+        const unsigned char* row_ptr = A.logits + row * A.vocab * A.elem_bytes;
+        const RowGeom geom = row_geom(row_ptr, A.vocab, A.elem_bytes);
+        if (x_valid) owner = owner_split(x, geom, A.chunk_vecs * (16 / A.elem_bytes), A.splits);
+    }
     packed = 0;
     bits = 0;
     draft_bits = 0;
@@ -470,7 +490,7 @@ __device__ __forceinline__ void combine_row(const ScanArgs& A, int64_t row, int3
         TilePartial tp[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            if (s0 + j < A.splits) tp[j] = parts[s0 + j];
+            if (s0 + j < A.splits) tp[j] = parts[(s0 + j) * stride];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             if (s0 + j < A.splits) {
@@ -503,7 +523,22 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
     const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
     if (i >= A.num_requests) return;
     const int32_t K = A.block_lens[i];
-    const int64_t o = A.offsets[i];
+    int64_t o;
+    if (A.offsets) {
+        o = A.offsets[i];
+    } else {
+        // Packed layout, few requests: this wavefront sums the row counts of
+        // the requests before it.
+        long long part = 0;
+#pragma unroll 4
+        for (int64_t j = lane; j < i; j += 64) {
+            const int32_t Kj = A.block_lens[j];
+            part += (long long)(Kj > 0 ? Kj : 0) + 1;
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
+        o = part;
+    }
     if (!(K >= 0 && o >= 0 && o + (int64_t)K < A.total_rows)) {
         if (lane == 0) {
             A.out_accept_len[i] = 0;
@@ -530,7 +565,7 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         float r = 0.0f;
         if (have) {
             const int64_t row = o + p;
-            if (A.splits == 1) {
+            if (A.partials == nullptr) {
                 const RowRecord rec = A.records[row];
                 y = rec.y_flags & kArgmaxMask;
                 mism = (rec.y_flags & kMismatchBit) != 0u;
@@ -590,6 +625,49 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
     }
 }
 
+// Packed row offsets for the calls that have no row kernel before the scan.
+__global__ __launch_bounds__(kRowThreads) void asd_offsets_kernel(
+    int32_t num_requests, const int32_t* __restrict__ block_lens, int64_t* __restrict__ offsets) {
+    write_packed_offsets(num_requests, block_lens, offsets);
+}
+
+ScanArgs scan_args(const CallArgs& a, int64_t rows, int64_t vocab, int elem_bytes) {
+    ScanArgs A{};
+    A.num_requests = a.num_requests;
+    A.request_blocks = (int32_t)((a.num_requests + kScanThreads / 64 - 1) / (kScanThreads / 64));
+    A.total_rows = rows;
+    A.vocab = vocab;
+    A.elem_bytes = elem_bytes;
+    A.logits = (const unsigned char*)a.logits;
+    A.draft_tokens = a.draft_tokens;
+    A.block_lens = a.block_lens;
+    A.offsets = a.row_offsets;
+    A.tau = a.tau;
+    A.exc_cap = a.exc_cap;
+    A.budget = a.budget;
+    A.out_accept_len = a.out_accept_len;
+    A.out_next_token = a.out_next_token;
+    A.out_regret = a.out_regret;
+    A.out_argmax = a.out_argmax;
+    return A;
+}
+
+hipError_t launch_scan(const ScanArgs& A, bool argmax_rows, hipStream_t stream) {
+    const int64_t row_blocks =
+        (argmax_rows && A.out_argmax) ? (A.total_rows + kScanThreads - 1) / kScanThreads : 0;
+    asd_scan_kernel<<<(unsigned)(A.request_blocks + row_blocks), kScanThreads, 0, stream>>>(A);
+    return hipGetLastError();
+}
+
+template <typename... Args>
+hipError_t launch_row(int elem_bytes, dim3 grid, hipStream_t stream, Args... args) {
+    if (elem_bytes == 2)
+        asd_row_kernel<2><<<grid, kRowThreads, 0, stream>>>(args...);
+    else
+        asd_row_kernel<4><<<grid, kRowThreads, 0, stream>>>(args...);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launch
@@ -603,42 +681,52 @@ hipError_t launch_verify(const Plan& plan, const CallArgs& a, void* workspace,
 
     const dim3 grid((unsigned)(plan.rows * plan.splits));
     int32_t* row_argmax = plan.splits == 1 ? a.out_argmax : nullptr;
-    if (plan.elem_bytes == 2)
-        asd_row_kernel<2><<<grid, kRowThreads, 0, stream>>>(
-            (const unsigned char*)a.logits, plan.vocab, plan.splits, plan.chunk_vecs,
-            a.draft_tokens, partials, records, row_argmax, a.num_requests, a.block_lens, packed);
-    else
-        asd_row_kernel<4><<<grid, kRowThreads, 0, stream>>>(
-            (const unsigned char*)a.logits, plan.vocab, plan.splits, plan.chunk_vecs,
-            a.draft_tokens, partials, records, row_argmax, a.num_requests, a.block_lens, packed);
-    hipError_t err = hipGetLastError();
+    hipError_t err = launch_row(plan.elem_bytes, grid, stream, (const unsigned char*)a.logits,
+                                plan.vocab, (int64_t)0, plan.splits, plan.chunk_vecs,
+                                a.draft_tokens, partials, records, row_argmax, a.num_requests,
+                                a.block_lens, packed);
     if (err != hipSuccess) return err;
 
-    ScanArgs A;
-    A.num_requests = a.num_requests;
-    A.request_blocks = (int32_t)((a.num_requests + kScanThreads / 64 - 1) / (kScanThreads / 64));
-    A.total_rows = plan.rows;
-    A.vocab = plan.vocab;
-    A.elem_bytes = plan.elem_bytes;
+    ScanArgs A = scan_args(a, plan.rows, plan.vocab, plan.elem_bytes);
     A.splits = plan.splits;
     A.chunk_vecs = plan.chunk_vecs;
-    A.logits = (const unsigned char*)a.logits;
-    A.draft_tokens = a.draft_tokens;
-    A.block_lens = a.block_lens;
     A.offsets = a.row_offsets ? a.row_offsets : packed;
-    A.tau = a.tau;
-    A.exc_cap = a.exc_cap;
-    A.budget = a.budget;
     A.records = records;
     A.partials = partials;
-    A.out_accept_len = a.out_accept_len;
-    A.out_next_token = a.out_next_token;
-    A.out_regret = a.out_regret;
-    A.out_argmax = a.out_argmax;
-    const int64_t row_blocks =
-        (plan.splits > 1 && a.out_argmax) ? (plan.rows + kScanThreads - 1) / kScanThreads : 0;
-    asd_scan_kernel<<<(unsigned)(A.request_blocks + row_blocks), kScanThreads, 0, stream>>>(A);
-    return hipGetLastError();
+    A.shard_vocab = 0;
+    return launch_scan(A, plan.splits > 1, stream);
+}
+
+hipError_t launch_shard_argmax(int elem_bytes, const void* shard_logits, int64_t shard_vocab,
+                               int64_t vocab_offset, int64_t rows, const int32_t* draft_tokens,
+                               void* out_partials, hipStream_t stream) {
+    const int64_t nvec = shard_vocab * elem_bytes / 16;
+    int64_t chunk = (nvec + kRowThreads - 1) / kRowThreads * kRowThreads;
+    if (chunk < kRowThreads) chunk = kRowThreads;
+    return launch_row(elem_bytes, dim3((unsigned)rows), stream,
+                      (const unsigned char*)shard_logits, shard_vocab, vocab_offset, 1, chunk,
+                      draft_tokens, (TilePartial*)out_partials, (RowRecord*)nullptr,
+                      (int32_t*)nullptr, (int32_t)0, (const int32_t*)nullptr,
+                      (int64_t*)nullptr);
+}
+
+hipError_t launch_verify_partials(const void* partials, int num_shards, int64_t shard_vocab,
+                                  int64_t vocab, int64_t rows, const CallArgs& a,
+                                  int64_t* packed_offsets, hipStream_t stream) {
+    if (!a.row_offsets && packed_offsets) {
+        asd_offsets_kernel<<<1, kRowThreads, 0, stream>>>(a.num_requests, a.block_lens,
+                                                          packed_offsets);
+        const hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
+    ScanArgs A = scan_args(a, rows, vocab, 2);
+    A.splits = num_shards;
+    A.chunk_vecs = 0;
+    A.offsets = a.row_offsets ? a.row_offsets : packed_offsets;   // NULL: summed per wavefront
+    A.records = nullptr;
+    A.partials = (const TilePartial*)partials;
+    A.shard_vocab = shard_vocab;
+    return launch_scan(A, true, stream);
 }
 
 }  // namespace asd

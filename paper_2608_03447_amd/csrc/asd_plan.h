@@ -74,4 +74,21 @@ Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int32_t num_requests
 hipError_t launch_verify(const Plan& plan, const CallArgs& args, void* workspace,
                          hipStream_t stream);
 
+// One vocabulary shard: rows of `shard_vocab` columns that are columns
+// [vocab_offset, vocab_offset + shard_vocab) of the full vocabulary.  Writes one
+// TilePartial per row.
+hipError_t launch_shard_argmax(int elem_bytes, const void* shard_logits, int64_t shard_vocab,
+                               int64_t vocab_offset, int64_t rows, const int32_t* draft_tokens,
+                               void* out_partials, hipStream_t stream);
+
+// Combine the partials of `num_shards` shards ([shard][row], shard k holding
+// columns [k shard_vocab, (k + 1) shard_vocab)) and run Algorithm 1.
+// `packed_offsets` (int64 [num_requests]) is scratch for the packed layout; when
+// it is NULL too, each scan wavefront sums its request's offset itself (meant
+// for at most kWaveOffsetsMaxRequests requests).
+constexpr int32_t kWaveOffsetsMaxRequests = 1024;
+hipError_t launch_verify_partials(const void* partials, int num_shards, int64_t shard_vocab,
+                                  int64_t vocab, int64_t rows, const CallArgs& args,
+                                  int64_t* packed_offsets, hipStream_t stream);
+
 }  // namespace asd

@@ -88,3 +88,64 @@ def test_package_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(asd, "LIBRARY", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         asd._load()
+
+
+def _shard(**kw):
+    lib = asd._load()
+    a = dict(logits=0x1000, dtype=1, width=100, offset=0, vocab=100, rows=2, draft=0x2000,
+             out=0x3000, stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_shard_argmax(vp(a["logits"]), a["dtype"], a["width"], a["offset"], a["vocab"],
+                                a["rows"], vp(a["draft"]), vp(a["out"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=5), 2),
+    (dict(width=0), 1),
+    (dict(offset=-1), 1),
+    (dict(offset=1), 1),                      # offset + width > vocab
+    (dict(vocab=1 << 30, width=10), 1),
+    (dict(rows=0), 1),
+    (dict(rows=1 << 31), 1),
+    (dict(logits=None), 1),
+    (dict(draft=None), 1),
+    (dict(out=None), 1),
+    (dict(out=0x3008), 1),                    # partials must be 16-byte aligned
+    (dict(logits=0x1001), 1),
+])
+def test_shard_argmax_rejects_invalid_arguments(kw, status):
+    assert _shard(**kw) == status
+
+
+def _vp(**kw):
+    lib = asd._load()
+    a = dict(parts=0x1000, shards=2, width=50, vocab=100, nreq=1, rows=2, draft=0x2000,
+             lens=0x3000, offs=None, tau=0x4000, cap=0x5000, budget=0x6000, acc=0x7000,
+             nxt=0x8000, amax=None, regret=None, stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_verify_partials(vp(a["parts"]), a["shards"], a["width"], a["vocab"], a["nreq"],
+                                   a["rows"], vp(a["draft"]), vp(a["lens"]), vp(a["offs"]),
+                                   vp(a["tau"]), vp(a["cap"]), vp(a["budget"]), vp(a["acc"]),
+                                   vp(a["nxt"]), vp(a["amax"]), vp(a["regret"]),
+                                   vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(shards=0), 1),
+    (dict(shards=4097), 1),
+    (dict(width=0), 1),
+    (dict(width=30), 1),                      # 2 x 30 < 100: columns left over
+    (dict(width=100), 1),                     # shard 2 would be empty
+    (dict(parts=None), 1),
+    (dict(parts=0x1004), 1),
+    (dict(lens=None), 1),
+    (dict(nreq=3, rows=2), 1),
+])
+def test_verify_partials_rejects_invalid_arguments(kw, status):
+    assert _vp(**kw) == status
+
+
+def test_verify_partials_empty_batch_is_a_no_op():
+    assert _vp(nreq=0, rows=0, parts=None, draft=None) == 0

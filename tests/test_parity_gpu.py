@@ -327,3 +327,87 @@ def test_without_optional_per_row_outputs(cfg):
     assert np.array_equal(acc.cpu().numpy(), r["accept_len"])
     assert np.array_equal(nxt.cpu().numpy(), r["next_token"])
     assert np.array_equal(budget.cpu().numpy().view(np.uint32), r["budget"].view(np.uint32))
+
+
+# ------------------------------------------ vocabulary-sharded verification
+
+def sharded_verify(logits, draft, lens, tau, cap, budget, num_shards, row_offsets=None):
+    """Split every row into num_shards column shards (equal widths, the last
+    narrower), reduce each shard separately, then finish from the partials."""
+    import paper_2608_03447_amd as asd
+    from asd_gpu import device_logits
+    dev = torch.device("cuda:0")
+    rows, vocab = logits.shape
+    width = -(-vocab // num_shards)
+    n = len(lens)
+    td = torch.from_numpy(np.ascontiguousarray(draft, dtype=np.int32)).to(dev)
+    parts = torch.empty((num_shards, rows, 4), dtype=torch.int32, device=dev)
+    full = device_logits(logits, dev)
+    for k in range(num_shards):
+        shard = full[:, k * width:min((k + 1) * width, vocab)].contiguous()
+        asd.asd_shard_argmax(shard, k * width, vocab, td, out_partials=parts[k])
+    tb = torch.from_numpy(np.array(budget, dtype=np.float32).reshape(n, 2)).to(dev)
+    amax = torch.full((rows,), -7, dtype=torch.int32, device=dev)
+    regret = torch.full((rows,), float("nan"), dtype=torch.float32, device=dev)
+    to = None if row_offsets is None else torch.from_numpy(
+        np.ascontiguousarray(row_offsets, dtype=np.int64)).to(dev)
+    acc, nxt = asd.asd_verify_partials(
+        parts, width, vocab, td, torch.from_numpy(np.asarray(lens, dtype=np.int32)).to(dev),
+        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.asarray(tau, np.float32), (n,)))).to(dev),
+        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.asarray(cap, np.int32), (n,)))).to(dev),
+        tb, row_offsets=to, out_argmax=amax, out_regret=regret)
+    torch.cuda.synchronize()
+    return {"accept_len": acc.cpu().numpy(), "next_token": nxt.cpu().numpy(),
+            "argmax": amax.cpu().numpy(), "regret": regret.cpu().numpy(),
+            "budget": tb.cpu().numpy()}
+
+
+@pytest.mark.parametrize("cfg,shards", [(3, 8), (3, 3), (4, 8), (5, 8), (5, 1), (2, 2)])
+def test_vocabulary_sharded_equals_unsharded(cfg, shards):
+    w = W.make_config(cfg, batch=None if cfg != 3 else 64)
+    print("case sharded config %d x %d shards" % (cfg, shards), flush=True)
+    g = sharded_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget, shards)
+    r = oracle_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
+    bad = mismatches(g, r)
+    assert not bad, "%s differs in %s: %s" % (w.name, bad, describe(g, r))
+
+
+@pytest.mark.parametrize("vocab,shards", [(1000, 7), (50257, 8), (17, 4), (9, 9), (300, 2)])
+def test_sharded_special_values_ragged_widths_and_offsets(vocab, shards):
+    rng = np.random.default_rng(vocab + shards)
+    for dtype in ("bf16", "f32"):
+        lens = rng.integers(0, 7, 6).astype(np.int32)
+        rows = int(np.sum(lens + 1)) + 3
+        offs = np.concatenate([[0], np.cumsum(lens + 1)[:-1]]).astype(np.int64) + 2
+        dyadic = (rng.integers(-6, 7, size=(rows, vocab)) / 4.0).astype(np.float32)
+        special = SPECIAL_BITS[rng.integers(0, len(SPECIAL_BITS), size=(rows, vocab))].view(np.float32)
+        z = np.where(rng.random((rows, vocab)) < 0.1, special, dyadic).astype(np.float32)
+        logits = (z.view(np.uint32) >> 16).astype(np.uint16) if dtype == "bf16" else z
+        zf = W.bf16_to_f32(logits) if dtype == "bf16" else logits
+        y = np.argmax(np.nan_to_num(zf, nan=-np.inf), axis=1)
+        draft = np.where(rng.random(rows) < 0.6, y, rng.integers(-1, vocab + 1, rows)).astype(np.int32)
+        budget = np.stack([rng.choice([0.0, 1.0, 4.0], 6), np.zeros(6)], axis=1).astype(np.float32)
+        g = sharded_verify(logits, draft, lens, 1.0, 2, budget, shards, row_offsets=offs)
+        r = oracle_verify(logits, draft, lens, 1.0, 2, budget, row_offsets=offs)
+        bad = mismatches(g, r)
+        assert not bad, "vocab %d shards %d %s differs in %s: %s" % (vocab, shards, dtype, bad,
+                                                                     describe(g, r))
+
+
+@pytest.mark.parametrize("num_requests", [1023, 1024, 1025, 3000])
+def test_sharded_packed_offsets_both_paths(num_requests):
+    """Up to 1,024 requests each scan wavefront sums its own packed offset;
+    above that a one-workgroup scan writes them first."""
+    rng = np.random.default_rng(num_requests)
+    vocab = 640
+    lens = rng.integers(0, 5, num_requests).astype(np.int32)
+    rows = int(np.sum(lens + 1))
+    z = rng.normal(0, 2, size=(rows, vocab)).astype(np.float32)
+    logits = W.f32_to_bf16(z)
+    y = np.argmax(W.bf16_to_f32(logits), axis=1)
+    draft = np.where(rng.random(rows) < 0.7, y, rng.integers(0, vocab, rows)).astype(np.int32)
+    budget = np.stack([rng.uniform(0, 6, num_requests), np.zeros(num_requests)], axis=1).astype(np.float32)
+    g = sharded_verify(logits, draft, lens, 2.0, 1, budget, 3)
+    r = oracle_verify(logits, draft, lens, 2.0, 1, budget)
+    bad = mismatches(g, r)
+    assert not bad, "%d requests differ in %s: %s" % (num_requests, bad, describe(g, r))
