@@ -101,6 +101,9 @@ def main():
                     help="bound on the CPU-oracle baseline's timed work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--opportunity", action="store_true",
+                    help="also accumulate the opportunity statistic (Eq. 4) every step, from "
+                         "the per-row argmax and regret the call writes")
     ap.add_argument("--shards", type=int, default=0,
                     help="vocabulary-sharded verification: split every row into this many "
                          "column shards held in separate buffers (as tensor-parallel ranks hold "
@@ -147,6 +150,23 @@ def main():
     def step():
         for lg, dr, a, x in calls:
             asd.asd_verify(lg, dr, lens, tau, cap, budget, out_accept_len=a, out_next_token=x)
+
+    if args.opportunity:
+        if w.blocks != 1 or args.shards:
+            raise SystemExit("--opportunity needs a single-call, unsharded workload")
+        row_amax = torch.empty(w.rows_per_call, dtype=torch.int32, device=dev)
+        row_reg = torch.empty(w.rows_per_call, dtype=torch.float32, device=dev)
+        taus = torch.tensor([0.5, 1.0, 2.0, 4.0, 8.0, float("inf")], dtype=torch.float32,
+                            device=dev)
+        ps = torch.tensor([0, 1, 2, 3, 4, 6, 8], dtype=torch.int32, device=dev)
+        opp_counts = torch.zeros((6, 7), dtype=torch.int64, device=dev)
+        opp_m = torch.zeros(1, dtype=torch.int64, device=dev)
+
+        def step():
+            asd.asd_verify(logits, draft, lens, tau, cap, budget, out_accept_len=acc[0],
+                           out_next_token=nxt[0], out_argmax=row_amax, out_regret=row_reg)
+            asd.asd_opportunity(draft, row_amax, row_reg, w.vocab, lens, taus, ps, opp_counts,
+                                opp_m)
 
     if args.shards > 0:
         if w.blocks != 1:
@@ -253,10 +273,13 @@ def main():
         tag += "_seq%d" % w.blocks
     if args.shards > 0:
         tag += "_shards%d" % args.shards
+    if args.opportunity:
+        tag += "_opportunity"
     traffic = read_traffic(tag, kernel_source_hash())
-    metric = METRIC if (args.config == 3 and not args.shards) else (
-        "verified logit rows/s + achieved HBM GB/s (%s%s)" % (
-            w.name, ", %d vocabulary shards" % args.shards if args.shards else ""))
+    metric = METRIC if (args.config == 3 and not args.shards and not args.opportunity) else (
+        "verified logit rows/s + achieved HBM GB/s (%s%s%s)" % (
+            w.name, ", %d vocabulary shards" % args.shards if args.shards else "",
+            ", with the opportunity statistic" if args.opportunity else ""))
     out = {
         "metric": metric,
         "value": rows_per_s,
@@ -279,7 +302,9 @@ def main():
                                     if w.blocks > 1 else "") +
                                    (", vocabulary split into %d column shards (asd_shard_argmax"
                                     " x %d + asd_verify_partials) on one GPU"
-                                    % (args.shards, args.shards) if args.shards else "")),
+                                    % (args.shards, args.shards) if args.shards else "") +
+                                   (", per-row argmax/regret written and the Eq. 4 opportunity"
+                                    " counts accumulated each step" if args.opportunity else "")),
                    "vocab_shards": args.shards or 1,
                    "calls_per_step": w.blocks,
                    "rows_per_call": w.rows_per_call, "vocab": w.vocab,

@@ -198,6 +198,33 @@ asd_status asd_verify_partials(const asd_row_partial *partials, int32_t num_shar
                                int32_t *out_next_token, int32_t *out_argmax,
                                float *out_regret, void *stream);
 
+/*
+ * asd_opportunity -- accumulate the opportunity statistic of Sec. 3.1, Eq. 4:
+ *   Omega(tau, p) = (1 / |M|) * #{ mismatch (x, i) in M : r_i <= tau,
+ *                    i + p <= K, and x_l = y*_l for l = i+1 .. i+p },
+ * the share of draft-target mismatches that have low regret and are followed
+ * by p target-greedy drafts, over the blocks of one verified batch.
+ *
+ * draft_tokens, block_lens, row_offsets, num_requests, total_rows, vocab
+ *                 as for asd_verify (the batch that was verified); row_offsets
+ *                 may be NULL (packed layout) only up to 1024 requests.
+ * row_argmax      int32 [total_rows]: the out_argmax of asd_verify on the batch.
+ * row_regret      float [total_rows]: the out_regret of asd_verify on the batch.
+ * taus            float [num_taus] (raw regret thresholds); ps int32 [num_ps],
+ *                 p >= 0; 1 <= num_taus * num_ps <= 1024.
+ * counts          uint64 [num_taus][num_ps]: count of contributing mismatches,
+ *                 added to in place (the numerator of Omega(taus[a], ps[b])).
+ * mismatches      uint64 [1]: |M|, added to in place.
+ * A draft id outside [0, V) is a mismatch (its regret is +inf).  Requests that
+ * asd_verify does not verify are skipped.  Allocates nothing; asynchronous.
+ */
+asd_status asd_opportunity(const int32_t *draft_tokens, const int32_t *row_argmax,
+                           const float *row_regret, int64_t vocab, int32_t num_requests,
+                           int64_t total_rows, const int32_t *block_lens,
+                           const int64_t *row_offsets, const float *taus, int32_t num_taus,
+                           const int32_t *ps, int32_t num_ps, uint64_t *counts,
+                           uint64_t *mismatches, void *stream);
+
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 

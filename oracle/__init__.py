@@ -39,6 +39,9 @@ def _load():
         lib.oracle_verify.argtypes = [vp, ctypes.c_int, i64, i32, i64, vp, vp, vp, vp, vp, vp,
                                       vp, vp, vp, vp]
         lib.oracle_verify.restype = ctypes.c_int
+        lib.oracle_opportunity.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, i32, vp, i32,
+                                           vp, vp]
+        lib.oracle_opportunity.restype = None
         _lib = lib
     return _lib
 
@@ -123,3 +126,25 @@ def verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets=N
         raise ValueError("oracle_verify rejected its arguments (code %d)" % rc)
     return {"accept_len": accept, "next_token": nxt, "budget": bud, "argmax": amax,
             "regret": regret}
+
+
+def opportunity(draft_tokens, row_argmax, row_regret, vocab, block_lens, taus, ps,
+                row_offsets=None):
+    """Eq. 4 counts over one batch: returns ``(counts[len(taus), len(ps)], |M|)``.
+
+    ``row_argmax`` / ``row_regret`` are the per-row outputs of :func:`verify`.
+    Omega(taus[a], ps[b]) = counts[a, b] / |M|.
+    """
+    draft = np.ascontiguousarray(draft_tokens, dtype=np.int32)
+    amax = np.ascontiguousarray(row_argmax, dtype=np.int32)
+    reg = np.ascontiguousarray(row_regret, dtype=np.float32)
+    lens = np.ascontiguousarray(block_lens, dtype=np.int32)
+    taus = np.ascontiguousarray(taus, dtype=np.float32)
+    ps = np.ascontiguousarray(ps, dtype=np.int32)
+    offs = None if row_offsets is None else np.ascontiguousarray(row_offsets, dtype=np.int64)
+    counts = np.zeros((taus.shape[0], ps.shape[0]), dtype=np.uint64)
+    mism = np.zeros(1, dtype=np.uint64)
+    _load().oracle_opportunity(_ptr(draft), _ptr(amax), _ptr(reg), int(vocab), lens.shape[0],
+                               draft.shape[0], _ptr(lens), _ptr(offs), _ptr(taus),
+                               taus.shape[0], _ptr(ps), ps.shape[0], _ptr(counts), _ptr(mism))
+    return counts, int(mism[0])

@@ -18,6 +18,7 @@
  *      Eq. 7 and the constraints of Eqs. 9-11); the longest all-true prefix
  *      a (Eq. 12); the ledger update s' = s + C_a (Sec. 3.3, Eq. 13); and the
  *      recovery token y*_{a+1} or, when a = K, the bonus token y*_{K+1}.
+ *   3. The opportunity statistic of Eq. 4 (Sec. 3.1) from the per-row outputs.
  *   Equations are numbered in the order the paper numbers them: 1 target rows,
  *   2 strict prefix, 3 local regret, 4 opportunity, 5 mismatch indicator,
  *   6 remaining length, 7 normalized gate, 8 cumulative state, 9 budget,
@@ -309,4 +310,63 @@ int oracle_verify(const void *logits, int dtype, int64_t vocab,
 
     free(y_all);
     return 0;
+}
+
+/* -------------------------------------------- opportunity statistic (Eq. 4) */
+
+/*
+ * Counts of the opportunity statistic of Sec. 3.1, Eq. 4, over the blocks of one
+ * batch, accumulated into counts[a * num_ps + b] (numerator of
+ * Omega(taus[a], ps[b])) and *mismatches (|M|).  Omega = numerator / |M|.
+ *
+ * M is the set of draft positions i (1-based, 1 <= i <= K) with x_i != y*_i
+ * (Eq. 5; a draft id outside [0, V) is a mismatch).  A mismatch contributes to
+ * (tau, p) when r_i <= tau, i + p <= K, and x_l = y*_l for every l in
+ * i+1 .. i+p.  y* and r are the per-row argmax and regret of a verifier call
+ * on the same batch (its out_argmax / out_regret).  Requests whose rows do not
+ * fit in [0, total_rows), or with K < 0, are not evaluated.
+ */
+void oracle_opportunity(const int32_t *draft, const int32_t *row_argmax,
+                        const float *row_regret, int64_t vocab,
+                        int32_t num_requests, int64_t total_rows,
+                        const int32_t *block_lens, const int64_t *row_offsets,
+                        const float *taus, int32_t num_taus,
+                        const int32_t *ps, int32_t num_ps,
+                        uint64_t *counts, uint64_t *mismatches)
+{
+    int64_t packed_offset = 0;
+    for (int32_t req = 0; req < num_requests; ++req) {
+        int32_t K = block_lens[req];
+        int64_t o = row_offsets ? row_offsets[req] : packed_offset;
+        packed_offset += (int64_t)(K > 0 ? K : 0) + 1;
+        if (K < 0 || o < 0 || o + (int64_t)K >= total_rows)
+            continue;
+        for (int32_t i = 1; i <= K; ++i) {
+            int64_t row = o + i - 1;
+            int32_t x = draft[row];
+            int is_mismatch = !(x >= 0 && (int64_t)x < vocab) || x != row_argmax[row];
+            if (!is_mismatch)
+                continue;
+            *mismatches += 1;
+            for (int32_t a = 0; a < num_taus; ++a) {
+                if (!(row_regret[row] <= taus[a]))
+                    continue;
+                for (int32_t b = 0; b < num_ps; ++b) {
+                    int32_t p = ps[b];
+                    int all_greedy = 1;
+                    if (!((int64_t)i + p <= (int64_t)K))
+                        continue;
+                    for (int32_t l = i + 1; l <= i + p; ++l) {
+                        int64_t lrow = o + l - 1;
+                        if (draft[lrow] != row_argmax[lrow]) {
+                            all_greedy = 0;
+                            break;
+                        }
+                    }
+                    if (all_greedy)
+                        counts[(int64_t)a * num_ps + b] += 1;
+                }
+            }
+        }
+    }
 }

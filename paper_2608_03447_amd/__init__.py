@@ -14,6 +14,7 @@ import torch
 from .build import LIBRARY
 
 __all__ = ["asd_verify", "asd_verify_ws", "asd_shard_argmax", "asd_verify_partials",
+           "asd_opportunity",
            "asd_workspace_bytes", "asd_status_string", "asd_version", "asd_release", "AsdError",
            "ASD_F32", "ASD_BF16", "library_path"]
 
@@ -53,6 +54,9 @@ def _load():
     lib.asd_verify_partials.argtypes = [vp, i32, i64, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp,
                                          vp, vp, vp, vp]
     lib.asd_verify_partials.restype = ctypes.c_int
+    lib.asd_opportunity.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, i32, vp, i32, vp, vp,
+                                     vp]
+    lib.asd_opportunity.restype = ctypes.c_int
     lib.asd_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i64]
     lib.asd_workspace_bytes.restype = sz
     lib.asd_status_string.argtypes = [ctypes.c_int]
@@ -249,3 +253,47 @@ def asd_verify_partials(partials, shard_vocab, vocab, draft_tokens, block_lens, 
     if st != 0:
         raise AsdError(st, "asd_verify_partials")
     return acc, nxt
+
+
+def asd_opportunity(draft_tokens, row_argmax, row_regret, vocab, block_lens, taus, ps, counts,
+                    mismatches, *, row_offsets=None):
+    """Accumulate the opportunity statistic of Eq. 4 (``asd_opportunity`` of ``include/asd.h``).
+
+    row_argmax / row_regret  the out_argmax / out_regret of asd_verify on the batch
+    taus   float32 [A]; ps int32 [P]
+    counts int64 [A, P] and mismatches int64 [1]: uint64 accumulators, added to in place
+    """
+    dev = draft_tokens.device
+    rows = draft_tokens.shape[0]
+    for t, name, dt, shape in ((draft_tokens, "draft_tokens", torch.int32, (rows,)),
+                               (row_argmax, "row_argmax", torch.int32, (rows,)),
+                               (row_regret, "row_regret", torch.float32, (rows,)),
+                               (taus, "taus", torch.float32, None),
+                               (ps, "ps", torch.int32, None),
+                               (mismatches, "mismatches", torch.int64, (1,))):
+        if t.dtype != dt or t.device != dev or not t.is_contiguous() or \
+                (shape is not None and t.shape != shape):
+            raise ValueError("%s must be a contiguous %s tensor%s on %s" % (
+                name, dt, "" if shape is None else " of shape %s" % (shape,), dev))
+    if block_lens.dtype != torch.int32 or block_lens.device != dev:
+        raise ValueError("block_lens must be an int32 tensor on %s" % dev)
+    n = block_lens.shape[0]
+    if counts.dtype != torch.int64 or counts.shape != (taus.shape[0], ps.shape[0]) \
+            or not counts.is_contiguous() or counts.device != dev:
+        raise ValueError("counts must be a contiguous int64 (%d, %d) tensor on %s"
+                         % (taus.shape[0], ps.shape[0], dev))
+    if row_offsets is not None and (row_offsets.dtype != torch.int64 or row_offsets.shape != (n,)):
+        raise ValueError("row_offsets must be int64 of shape (%d,)" % n)
+    block_lens = block_lens.contiguous()
+
+    def p(t):
+        return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+    with torch.cuda.device(dev):
+        st = _load().asd_opportunity(p(draft_tokens), p(row_argmax), p(row_regret), int(vocab), n,
+                                     rows, p(block_lens), p(row_offsets), p(taus),
+                                     taus.shape[0], p(ps), ps.shape[0], p(counts),
+                                     p(mismatches),
+                                     ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
+    if st != 0:
+        raise AsdError(st, "asd_opportunity")

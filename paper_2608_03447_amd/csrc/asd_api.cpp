@@ -305,6 +305,31 @@ asd_status asd_verify_partials(const asd_row_partial* partials, int32_t num_shar
                : ASD_EHIP;
 }
 
+asd_status asd_opportunity(const int32_t* draft_tokens, const int32_t* row_argmax,
+                           const float* row_regret, int64_t vocab, int32_t num_requests,
+                           int64_t total_rows, const int32_t* block_lens,
+                           const int64_t* row_offsets, const float* taus, int32_t num_taus,
+                           const int32_t* ps, int32_t num_ps, uint64_t* counts,
+                           uint64_t* mismatches, void* stream) {
+    if (vocab < 1 || vocab >= ((int64_t)1 << 30)) return ASD_EINVAL;
+    if (num_requests < 0 || total_rows < (int64_t)num_requests ||
+        total_rows >= ((int64_t)1 << 31))
+        return ASD_EINVAL;
+    if (num_taus < 1 || num_ps < 1 || (int64_t)num_taus * num_ps > kMaxOpportunityPairs)
+        return ASD_EINVAL;
+    if (num_requests == 0) return ASD_OK;
+    if (!draft_tokens || !row_argmax || !row_regret || !block_lens || !taus || !ps || !counts ||
+        !mismatches)
+        return ASD_EINVAL;
+    if (!row_offsets && num_requests > kWaveOffsetsMaxRequests) return ASD_EINVAL;
+    return launch_opportunity(draft_tokens, row_argmax, row_regret, vocab, num_requests,
+                              total_rows, block_lens, row_offsets, taus, num_taus, ps, num_ps,
+                              (unsigned long long*)counts, (unsigned long long*)mismatches,
+                              (hipStream_t)stream) == hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
 const char* asd_status_string(asd_status status) {
     switch (status) {
         case ASD_OK: return "ASD_OK";

@@ -668,6 +668,100 @@ hipError_t launch_row(int elem_bytes, dim3 grid, hipStream_t stream, Args... arg
     return hipGetLastError();
 }
 
+// --------------------------------------------- opportunity statistic (Eq. 4)
+
+// Counts of Eq. 4 over one batch, one wavefront per request with lanes =
+// draft positions.  The ballot of target-greedy drafts gives, for every
+// position, the length of the run of greedy drafts that follows it (trailing
+// ones of the mask above the position, carried across 64-position chunks from
+// the block's end).  A mismatch at position i with r_i <= tau and a following
+// run of at least p greedy drafts (which also gives i + p <= K) counts for
+// (tau, p); each (tau, p) count of a chunk is one ballot's popcount.  Counts
+// gather in LDS, then in the caller's uint64 accumulators.
+__global__ __launch_bounds__(kScanThreads) void asd_opportunity_kernel(
+    const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ row_argmax,
+    const float* __restrict__ row_regret, int64_t vocab, int32_t num_requests,
+    int64_t total_rows, const int32_t* __restrict__ block_lens,
+    const int64_t* __restrict__ row_offsets, const float* __restrict__ taus, int32_t num_taus,
+    const int32_t* __restrict__ ps, int32_t num_ps, unsigned long long* __restrict__ counts,
+    unsigned long long* __restrict__ mismatches) {
+    __shared__ uint32_t s_counts[kMaxOpportunityPairs];
+    __shared__ uint32_t s_mism;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int pairs = num_taus * num_ps;
+    for (int k = tid; k < pairs; k += kScanThreads) s_counts[k] = 0u;
+    if (tid == 0) s_mism = 0u;
+    __syncthreads();
+
+    const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
+    if (i < num_requests) {
+        const int32_t K = block_lens[i];
+        int64_t o;
+        if (row_offsets) {
+            o = row_offsets[i];
+        } else {                                      // packed: sum the earlier blocks
+            long long part = 0;
+            for (int64_t j = lane; j < i; j += 64) {
+                const int32_t Kj = block_lens[j];
+                part += (long long)(Kj > 0 ? Kj : 0) + 1;
+            }
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
+            o = part;
+        }
+        if (K >= 0 && o >= 0 && o + (int64_t)K < total_rows) {
+            // Chunks from the block's end: `carry` = greedy run starting at the
+            // first position after the chunk.
+            int64_t carry = 0;
+            uint32_t mism_total = 0;
+            const int64_t nchunks = ((int64_t)K + 63) / 64;
+            for (int64_t c = nchunks - 1; c >= 0; --c) {
+                const int64_t p = c * 64 + lane;      // 0-based draft position
+                const bool have = p < K;
+                bool match = false;
+                float r = 0.0f;
+                if (have) {
+                    const int32_t x = draft_tokens[o + p];
+                    match = x >= 0 && (int64_t)x < vocab && x == row_argmax[o + p];
+                    r = row_regret[o + p];
+                }
+                const unsigned long long m = __ballot(have && match);
+                const int n_here = (int)min((int64_t)64, (int64_t)K - c * 64);
+                // trailing ones of the mask above this lane, within the chunk
+                const unsigned long long above = lane < 63 ? (m >> (lane + 1)) : 0ull;
+                const int ones = (int)__builtin_ctzll(~above);   // < 64 - lane
+                const int64_t run = (lane + 1 + ones >= n_here) ? (int64_t)(n_here - 1 - lane) + carry
+                                                                : (int64_t)ones;
+                const bool mism = have && !match;
+                const unsigned long long mm = __ballot(mism);
+                mism_total += (uint32_t)__builtin_popcountll(mm);
+                if (mm) {
+                    for (int a = 0; a < num_taus; ++a) {
+                        const float t = taus[a];
+                        const unsigned long long ma = __ballot(mism && r <= t);
+                        if (!ma) continue;
+                        for (int b = 0; b < num_ps; ++b) {
+                            const int64_t need = ps[b];
+                            const unsigned long long mab = __ballot(mism && r <= t && run >= need);
+                            if (lane == 0 && mab)
+                                atomicAdd(&s_counts[a * num_ps + b],
+                                          (uint32_t)__builtin_popcountll(mab));
+                        }
+                    }
+                }
+                // greedy run starting at this chunk's first position
+                const int lead = m == ~0ull ? 64 : (int)__builtin_ctzll(~m);
+                carry = lead >= n_here ? (int64_t)n_here + carry : (int64_t)lead;
+            }
+            if (lane == 0 && mism_total) atomicAdd(&s_mism, mism_total);
+        }
+    }
+    __syncthreads();
+    for (int k = tid; k < pairs; k += kScanThreads)
+        if (s_counts[k]) atomicAdd(counts + k, (unsigned long long)s_counts[k]);
+    if (tid == 0 && s_mism) atomicAdd(mismatches, (unsigned long long)s_mism);
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launch
@@ -727,6 +821,20 @@ hipError_t launch_verify_partials(const void* partials, int num_shards, int64_t 
     A.partials = (const TilePartial*)partials;
     A.shard_vocab = shard_vocab;
     return launch_scan(A, true, stream);
+}
+
+hipError_t launch_opportunity(const int32_t* draft_tokens, const int32_t* row_argmax,
+                              const float* row_regret, int64_t vocab, int32_t num_requests,
+                              int64_t total_rows, const int32_t* block_lens,
+                              const int64_t* row_offsets, const float* taus, int32_t num_taus,
+                              const int32_t* ps, int32_t num_ps, unsigned long long* counts,
+                              unsigned long long* mismatches, hipStream_t stream) {
+    const unsigned blocks =
+        (unsigned)((num_requests + kScanThreads / 64 - 1) / (kScanThreads / 64));
+    asd_opportunity_kernel<<<blocks, kScanThreads, 0, stream>>>(
+        draft_tokens, row_argmax, row_regret, vocab, num_requests, total_rows, block_lens,
+        row_offsets, taus, num_taus, ps, num_ps, counts, mismatches);
+    return hipGetLastError();
 }
 
 }  // namespace asd

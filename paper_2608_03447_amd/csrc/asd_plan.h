@@ -91,4 +91,14 @@ hipError_t launch_verify_partials(const void* partials, int num_shards, int64_t 
                                   int64_t vocab, int64_t rows, const CallArgs& args,
                                   int64_t* packed_offsets, hipStream_t stream);
 
+// Opportunity statistic (Eq. 4): at most this many (tau, p) pairs per call.
+constexpr int kMaxOpportunityPairs = 1024;
+
+hipError_t launch_opportunity(const int32_t* draft_tokens, const int32_t* row_argmax,
+                              const float* row_regret, int64_t vocab, int32_t num_requests,
+                              int64_t total_rows, const int32_t* block_lens,
+                              const int64_t* row_offsets, const float* taus, int32_t num_taus,
+                              const int32_t* ps, int32_t num_ps, unsigned long long* counts,
+                              unsigned long long* mismatches, hipStream_t stream);
+
 }  // namespace asd

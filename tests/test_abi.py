@@ -149,3 +149,29 @@ def test_verify_partials_rejects_invalid_arguments(kw, status):
 
 def test_verify_partials_empty_batch_is_a_no_op():
     assert _vp(nreq=0, rows=0, parts=None, draft=None) == 0
+
+
+def _opp(**kw):
+    lib = asd._load()
+    a = dict(draft=0x1000, amax=0x2000, reg=0x3000, vocab=100, nreq=1, rows=2, lens=0x4000,
+             offs=None, taus=0x5000, ntau=2, ps=0x6000, nps=3, counts=0x7000, mism=0x8000,
+             stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_opportunity(vp(a["draft"]), vp(a["amax"]), vp(a["reg"]), a["vocab"], a["nreq"],
+                               a["rows"], vp(a["lens"]), vp(a["offs"]), vp(a["taus"]), a["ntau"],
+                               vp(a["ps"]), a["nps"], vp(a["counts"]), vp(a["mism"]),
+                               vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(vocab=0), 1), (dict(ntau=0), 1), (dict(nps=0), 1), (dict(ntau=33, nps=32), 1),
+    (dict(nreq=3, rows=2), 1), (dict(draft=None), 1), (dict(amax=None), 1), (dict(reg=None), 1),
+    (dict(counts=None), 1), (dict(mism=None), 1), (dict(taus=None), 1), (dict(ps=None), 1),
+])
+def test_opportunity_rejects_invalid_arguments(kw, status):
+    assert _opp(**kw) == status
+
+
+def test_opportunity_empty_batch_is_a_no_op():
+    assert _opp(nreq=0, rows=0, draft=None) == 0
