@@ -101,6 +101,9 @@ def main():
                     help="bound on the CPU-oracle baseline's timed work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="a step is every call of the workload followed by its commit "
+                         "(asd_commit), captured once as a HIP graph and replayed")
     ap.add_argument("--opportunity", action="store_true",
                     help="also accumulate the opportunity statistic (Eq. 4) every step, from "
                          "the per-row argmax and regret the call writes")
@@ -151,6 +154,33 @@ def main():
         for lg, dr, a, x in calls:
             asd.asd_verify(lg, dr, lens, tau, cap, budget, out_accept_len=a, out_next_token=x)
 
+    graph = None
+    if args.graph:
+        if args.shards or args.opportunity:
+            raise SystemExit("--graph runs the plain verifier calls")
+        nbytes = asd.asd_workspace_bytes(logits.dtype, w.vocab, w.num_requests, n)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        capacity = (args.warmup + args.steps + 2) * w.blocks * (int(w.block_lens.max()) + 1)
+        tokens = torch.zeros((w.num_requests, capacity), dtype=torch.int32, device=dev)
+        seq_len = torch.zeros(w.num_requests, dtype=torch.int64, device=dev)
+
+        def eager_step():
+            for lg, dr, a, x in calls:
+                asd.asd_verify_ws(lg, dr, lens, tau, cap, budget, ws, out_accept_len=a,
+                                  out_next_token=x)
+                asd.asd_commit(dr, lens, a, x, tokens, seq_len)
+
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(torch.cuda.current_stream(dev))
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            eager_step()
+        torch.cuda.synchronize()
+
+        def step():
+            graph.replay()
+
     if args.opportunity:
         if w.blocks != 1 or args.shards:
             raise SystemExit("--opportunity needs a single-call, unsharded workload")
@@ -189,6 +219,9 @@ def main():
     torch.cuda.synchronize()
     gpu_out = (acc.cpu().numpy().copy(), nxt.cpu().numpy().copy(),
                budget.cpu().numpy().copy())
+    gpu_commit = None
+    if args.graph:
+        gpu_commit = (tokens.cpu().numpy().copy(), seq_len.cpu().numpy().copy())
 
     for _ in range(args.warmup):
         step()
@@ -248,6 +281,14 @@ def main():
                 nxts.append(r["next_token"])
             return np.stack(accs), np.stack(nxts), ledger
 
+        def oracle_commits(accs, nxts):
+            tok = np.zeros(gpu_commit[0].shape, np.int32)
+            sl = np.zeros(w.num_requests, np.int64)
+            for b in range(w.blocks):
+                lg, dr = w.call(b)
+                tok, sl, _ = oracle.commit(dr, w.block_lens, accs[b], nxts[b], tok, sl)
+            return tok, sl
+
         times = []
         ref = None
         while True:
@@ -259,6 +300,9 @@ def main():
         med = statistics.median(times)
         ok = (np.array_equal(gpu_out[0], ref[0]) and np.array_equal(gpu_out[1], ref[1]) and
               np.array_equal(gpu_out[2].view(np.uint32), ref[2].view(np.uint32)))
+        if gpu_commit is not None:
+            r_tok, r_sl = oracle_commits(ref[0], ref[1])
+            ok = ok and np.array_equal(gpu_commit[0], r_tok) and np.array_equal(gpu_commit[1], r_sl)
         parity = "bit-exact" if ok else "MISMATCH"
         rows_step = w.rows_per_call * w.blocks
         cpu = {"value": rows_step / med, "unit": "rows/s", "cores": 1, "kind": "oracle",
@@ -275,11 +319,15 @@ def main():
         tag += "_shards%d" % args.shards
     if args.opportunity:
         tag += "_opportunity"
+    if args.graph:
+        tag += "_graph"
     traffic = read_traffic(tag, kernel_source_hash())
-    metric = METRIC if (args.config == 3 and not args.shards and not args.opportunity) else (
-        "verified logit rows/s + achieved HBM GB/s (%s%s%s)" % (
+    metric = METRIC if (args.config == 3 and not args.shards and not args.opportunity
+                        and not args.graph) else (
+        "verified logit rows/s + achieved HBM GB/s (%s%s%s%s)" % (
             w.name, ", %d vocabulary shards" % args.shards if args.shards else "",
-            ", with the opportunity statistic" if args.opportunity else ""))
+            ", with the opportunity statistic" if args.opportunity else "",
+            ", graph-captured rounds with commit" if args.graph else ""))
     out = {
         "metric": metric,
         "value": rows_per_s,
@@ -304,7 +352,9 @@ def main():
                                     " x %d + asd_verify_partials) on one GPU"
                                     % (args.shards, args.shards) if args.shards else "") +
                                    (", per-row argmax/regret written and the Eq. 4 opportunity"
-                                    " counts accumulated each step" if args.opportunity else "")),
+                                    " counts accumulated each step" if args.opportunity else "") +
+                                   (", every call followed by asd_commit, the step captured as"
+                                    " one HIP graph and replayed" if args.graph else "")),
                    "vocab_shards": args.shards or 1,
                    "calls_per_step": w.blocks,
                    "rows_per_call": w.rows_per_call, "vocab": w.vocab,

@@ -225,6 +225,31 @@ asd_status asd_opportunity(const int32_t *draft_tokens, const int32_t *row_argma
                            const int32_t *ps, int32_t num_ps, uint64_t *counts,
                            uint64_t *mismatches, void *stream);
 
+/*
+ * asd_commit -- the commit that follows verification (Sec. 3.3): request i
+ * emits its accepted drafts x_1..x_a followed by y*_{a+1} (Algorithm 1's
+ * return), and its committed sequence -- the extent its target and draft caches
+ * keep -- advances along exactly those a + 1 tokens.
+ *
+ * draft_tokens, block_lens, row_offsets, num_requests, total_rows
+ *                 as for the asd_verify call (row_offsets may be NULL, the packed
+ *                 layout, only up to 1024 requests).
+ * accept_len, next_token   the outputs of that call.
+ * tokens          int32 [num_requests][capacity]: entries
+ *                 [seq_len_i, seq_len_i + a_i + 1) of row i are written.
+ * seq_len         int64 [num_requests]: committed lengths, advanced in place.
+ * out_committed   int32 [num_requests] or NULL: a_i + 1, or 0 for a request that
+ *                 commits nothing.
+ * A request commits nothing when its rows do not fit in [0, total_rows), its
+ * next_token is negative (not verified), a_i lies outside [0, K_i], seq_len_i is
+ * negative, or the a_i + 1 tokens do not fit below capacity.  Allocates nothing;
+ * asynchronous on `stream`, so it can follow asd_verify in one captured graph.
+ */
+asd_status asd_commit(const int32_t *draft_tokens, const int32_t *block_lens,
+                      const int64_t *row_offsets, int32_t num_requests, int64_t total_rows,
+                      const int32_t *accept_len, const int32_t *next_token, int32_t *tokens,
+                      int64_t capacity, int64_t *seq_len, int32_t *out_committed, void *stream);
+
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 

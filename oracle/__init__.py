@@ -42,6 +42,8 @@ def _load():
         lib.oracle_opportunity.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, i32, vp, i32,
                                            vp, vp]
         lib.oracle_opportunity.restype = None
+        lib.oracle_commit.argtypes = [vp, vp, vp, i32, i64, vp, vp, vp, i64, vp, vp]
+        lib.oracle_commit.restype = None
         _lib = lib
     return _lib
 
@@ -148,3 +150,19 @@ def opportunity(draft_tokens, row_argmax, row_regret, vocab, block_lens, taus, p
                                draft.shape[0], _ptr(lens), _ptr(offs), _ptr(taus),
                                taus.shape[0], _ptr(ps), ps.shape[0], _ptr(counts), _ptr(mism))
     return counts, int(mism[0])
+
+
+def commit(draft_tokens, block_lens, accept_len, next_token, tokens, seq_len, row_offsets=None):
+    """Commit the emitted tokens (Sec. 3.3).  Returns new ``(tokens, seq_len, committed)``;
+    ``tokens`` is [num_requests, capacity] int32, ``seq_len`` int64 [num_requests]."""
+    draft = np.ascontiguousarray(draft_tokens, dtype=np.int32)
+    lens = np.ascontiguousarray(block_lens, dtype=np.int32)
+    acc = np.ascontiguousarray(accept_len, dtype=np.int32)
+    nxt = np.ascontiguousarray(next_token, dtype=np.int32)
+    tok = np.array(tokens, dtype=np.int32, copy=True)
+    sl = np.array(seq_len, dtype=np.int64, copy=True)
+    offs = None if row_offsets is None else np.ascontiguousarray(row_offsets, dtype=np.int64)
+    done = np.zeros(lens.shape[0], dtype=np.int32)
+    _load().oracle_commit(_ptr(draft), _ptr(lens), _ptr(offs), lens.shape[0], draft.shape[0],
+                          _ptr(acc), _ptr(nxt), _ptr(tok), tok.shape[1], _ptr(sl), _ptr(done))
+    return tok, sl, done

@@ -19,6 +19,8 @@
  *      a (Eq. 12); the ledger update s' = s + C_a (Sec. 3.3, Eq. 13); and the
  *      recovery token y*_{a+1} or, when a = K, the bonus token y*_{K+1}.
  *   3. The opportunity statistic of Eq. 4 (Sec. 3.1) from the per-row outputs.
+ *   4. The commit of the emitted tokens that keeps the caches on the emitted
+ *      sequence (Sec. 3.3).
  *   Equations are numbered in the order the paper numbers them: 1 target rows,
  *   2 strict prefix, 3 local regret, 4 opportunity, 5 mismatch indicator,
  *   6 remaining length, 7 normalized gate, 8 cumulative state, 9 budget,
@@ -368,5 +370,49 @@ void oracle_opportunity(const int32_t *draft, const int32_t *row_argmax,
                 }
             }
         }
+    }
+}
+
+/* ------------------------------------------------------- commit (Sec. 3.3) */
+
+/*
+ * The commit that follows verification (Sec. 3.3): request i emits its
+ * accepted drafts x_1..x_a followed by y*_{a+1} (Algorithm 1's return), and
+ * its committed sequence -- the length that the target and draft caches keep
+ * -- advances along exactly those a + 1 tokens.
+ *
+ * tokens     [num_requests][capacity] committed tokens of each request
+ * seq_len    [num_requests] committed length, advanced in place by a + 1
+ * committed  [num_requests] or NULL: tokens committed this round (a + 1), or 0
+ * A request whose rows do not fit in [0, total_rows), with next_token < 0 (not
+ * verified), with a outside [0, K], with seq_len < 0, or whose a + 1 tokens do
+ * not fit in [seq_len, capacity), commits nothing.
+ */
+void oracle_commit(const int32_t *draft, const int32_t *block_lens,
+                   const int64_t *row_offsets, int32_t num_requests,
+                   int64_t total_rows,
+                   const int32_t *accept_len, const int32_t *next_token,
+                   int32_t *tokens, int64_t capacity, int64_t *seq_len,
+                   int32_t *committed)
+{
+    int64_t packed_offset = 0;
+    for (int32_t i = 0; i < num_requests; ++i) {
+        int32_t K = block_lens[i];
+        int64_t o = row_offsets ? row_offsets[i] : packed_offset;
+        int32_t a = accept_len[i];
+        int64_t L = seq_len[i];
+        packed_offset += (int64_t)(K > 0 ? K : 0) + 1;
+        if (committed)
+            committed[i] = 0;
+        if (K < 0 || o < 0 || o + (int64_t)K >= total_rows)
+            continue;                          /* rows of a request asd_verify skips */
+        if (next_token[i] < 0 || L < 0 || a < 0 || a > K || L + a + 1 > capacity)
+            continue;
+        for (int32_t p = 0; p < a; ++p)
+            tokens[(int64_t)i * capacity + L + p] = draft[o + p];
+        tokens[(int64_t)i * capacity + L + a] = next_token[i];
+        seq_len[i] = L + a + 1;
+        if (committed)
+            committed[i] = a + 1;
     }
 }

@@ -14,7 +14,7 @@ import torch
 from .build import LIBRARY
 
 __all__ = ["asd_verify", "asd_verify_ws", "asd_shard_argmax", "asd_verify_partials",
-           "asd_opportunity",
+           "asd_opportunity", "asd_commit",
            "asd_workspace_bytes", "asd_status_string", "asd_version", "asd_release", "AsdError",
            "ASD_F32", "ASD_BF16", "library_path"]
 
@@ -57,6 +57,8 @@ def _load():
     lib.asd_opportunity.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, i32, vp, i32, vp, vp,
                                      vp]
     lib.asd_opportunity.restype = ctypes.c_int
+    lib.asd_commit.argtypes = [vp, vp, vp, i32, i64, vp, vp, vp, i64, vp, vp, vp]
+    lib.asd_commit.restype = ctypes.c_int
     lib.asd_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i64]
     lib.asd_workspace_bytes.restype = sz
     lib.asd_status_string.argtypes = [ctypes.c_int]
@@ -297,3 +299,41 @@ def asd_opportunity(draft_tokens, row_argmax, row_regret, vocab, block_lens, tau
                                      ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
     if st != 0:
         raise AsdError(st, "asd_opportunity")
+
+
+def asd_commit(draft_tokens, block_lens, accept_len, next_token, tokens, seq_len, *,
+               row_offsets=None, out_committed=None):
+    """Commit the emitted tokens (``asd_commit`` of ``include/asd.h``).
+
+    tokens   int32 [num_requests, capacity]; seq_len int64 [num_requests], both updated in place
+    """
+    dev = draft_tokens.device
+    n = block_lens.shape[0]
+    for t, name, dt, shape in ((draft_tokens, "draft_tokens", torch.int32, None),
+                               (block_lens, "block_lens", torch.int32, (n,)),
+                               (accept_len, "accept_len", torch.int32, (n,)),
+                               (next_token, "next_token", torch.int32, (n,)),
+                               (seq_len, "seq_len", torch.int64, (n,))):
+        if t.dtype != dt or t.device != dev or not t.is_contiguous() or \
+                (shape is not None and t.shape != shape):
+            raise ValueError("%s must be a contiguous %s tensor%s on %s" % (
+                name, dt, "" if shape is None else " of shape %s" % (shape,), dev))
+    if tokens.dtype != torch.int32 or tokens.dim() != 2 or tokens.shape[0] != n \
+            or not tokens.is_contiguous() or tokens.device != dev:
+        raise ValueError("tokens must be a contiguous int32 (%d, capacity) tensor on %s" % (n, dev))
+    if out_committed is not None and (out_committed.dtype != torch.int32
+                                      or out_committed.shape != (n,)):
+        raise ValueError("out_committed must be int32 of shape (%d,)" % n)
+    if row_offsets is not None and (row_offsets.dtype != torch.int64 or row_offsets.shape != (n,)):
+        raise ValueError("row_offsets must be int64 of shape (%d,)" % n)
+
+    def p(t):
+        return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+    with torch.cuda.device(dev):
+        st = _load().asd_commit(p(draft_tokens), p(block_lens), p(row_offsets), n,
+                                draft_tokens.shape[0], p(accept_len), p(next_token), p(tokens),
+                                tokens.shape[1], p(seq_len), p(out_committed),
+                                ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
+    if st != 0:
+        raise AsdError(st, "asd_commit")

@@ -330,6 +330,25 @@ asd_status asd_opportunity(const int32_t* draft_tokens, const int32_t* row_argma
                : ASD_EHIP;
 }
 
+asd_status asd_commit(const int32_t* draft_tokens, const int32_t* block_lens,
+                      const int64_t* row_offsets, int32_t num_requests, int64_t total_rows,
+                      const int32_t* accept_len, const int32_t* next_token, int32_t* tokens,
+                      int64_t capacity, int64_t* seq_len, int32_t* out_committed, void* stream) {
+    if (num_requests < 0 || total_rows < (int64_t)num_requests ||
+        total_rows >= ((int64_t)1 << 31) || capacity < 1)
+        return ASD_EINVAL;
+    if (num_requests == 0) return ASD_OK;
+    if (!draft_tokens || !block_lens || !accept_len || !next_token || !tokens || !seq_len)
+        return ASD_EINVAL;
+    if (!row_offsets && num_requests > kWaveOffsetsMaxRequests) return ASD_EINVAL;
+    if (capacity > INT64_MAX / num_requests) return ASD_EINVAL;
+    return launch_commit(draft_tokens, block_lens, row_offsets, num_requests, total_rows,
+                         accept_len, next_token, tokens, capacity, seq_len, out_committed,
+                         (hipStream_t)stream) == hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
 const char* asd_status_string(asd_status status) {
     switch (status) {
         case ASD_OK: return "ASD_OK";

@@ -762,6 +762,50 @@ __global__ __launch_bounds__(kScanThreads) void asd_opportunity_kernel(
     if (tid == 0 && s_mism) atomicAdd(mismatches, (unsigned long long)s_mism);
 }
 
+// --------------------------------------------------------- commit (Sec. 3.3)
+
+// The commit after verification: request i appends its emitted tokens x_1..x_a
+// and y*_{a+1} to its token buffer at its committed length and advances that
+// length (the extent the target and draft caches keep) by a + 1.  One
+// wavefront per request, lanes writing consecutive tokens.
+__global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
+    const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ block_lens,
+    const int64_t* __restrict__ row_offsets, int32_t num_requests, int64_t total_rows,
+    const int32_t* __restrict__ accept_len, const int32_t* __restrict__ next_token,
+    int32_t* __restrict__ tokens, int64_t capacity, int64_t* __restrict__ seq_len,
+    int32_t* __restrict__ committed) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
+    if (i >= num_requests) return;
+    const int32_t K = block_lens[i];
+    int64_t o;
+    if (row_offsets) {
+        o = row_offsets[i];
+    } else {                                          // packed: sum the earlier blocks
+        long long part = 0;
+        for (int64_t j = lane; j < i; j += 64) {
+            const int32_t Kj = block_lens[j];
+            part += (long long)(Kj > 0 ? Kj : 0) + 1;
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
+        o = part;
+    }
+    const int32_t a = accept_len[i];
+    const int32_t next = next_token[i];
+    const int64_t L = seq_len[i];
+    const bool ok = K >= 0 && o >= 0 && o + (int64_t)K < total_rows && next >= 0 && L >= 0 &&
+                    a >= 0 && a <= K && L + (int64_t)a + 1 <= capacity;
+    if (ok) {
+        int32_t* dst = tokens + i * capacity + L;
+        for (int64_t j = lane; j <= a; j += 64) dst[j] = j < a ? draft_tokens[o + j] : next;
+    }
+    if (lane == 0) {
+        if (ok) seq_len[i] = L + (int64_t)a + 1;
+        if (committed) committed[i] = ok ? a + 1 : 0;
+    }
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launch
@@ -834,6 +878,19 @@ hipError_t launch_opportunity(const int32_t* draft_tokens, const int32_t* row_ar
     asd_opportunity_kernel<<<blocks, kScanThreads, 0, stream>>>(
         draft_tokens, row_argmax, row_regret, vocab, num_requests, total_rows, block_lens,
         row_offsets, taus, num_taus, ps, num_ps, counts, mismatches);
+    return hipGetLastError();
+}
+
+hipError_t launch_commit(const int32_t* draft_tokens, const int32_t* block_lens,
+                         const int64_t* row_offsets, int32_t num_requests, int64_t total_rows,
+                         const int32_t* accept_len, const int32_t* next_token, int32_t* tokens,
+                         int64_t capacity, int64_t* seq_len, int32_t* committed,
+                         hipStream_t stream) {
+    const unsigned blocks =
+        (unsigned)((num_requests + kScanThreads / 64 - 1) / (kScanThreads / 64));
+    asd_commit_kernel<<<blocks, kScanThreads, 0, stream>>>(
+        draft_tokens, block_lens, row_offsets, num_requests, total_rows, accept_len, next_token,
+        tokens, capacity, seq_len, committed);
     return hipGetLastError();
 }
 

@@ -101,4 +101,10 @@ hipError_t launch_opportunity(const int32_t* draft_tokens, const int32_t* row_ar
                               const int32_t* ps, int32_t num_ps, unsigned long long* counts,
                               unsigned long long* mismatches, hipStream_t stream);
 
+hipError_t launch_commit(const int32_t* draft_tokens, const int32_t* block_lens,
+                         const int64_t* row_offsets, int32_t num_requests, int64_t total_rows,
+                         const int32_t* accept_len, const int32_t* next_token, int32_t* tokens,
+                         int64_t capacity, int64_t* seq_len, int32_t* committed,
+                         hipStream_t stream);
+
 }  // namespace asd

@@ -175,3 +175,23 @@ def test_opportunity_rejects_invalid_arguments(kw, status):
 
 def test_opportunity_empty_batch_is_a_no_op():
     assert _opp(nreq=0, rows=0, draft=None) == 0
+
+
+def _commit(**kw):
+    lib = asd._load()
+    a = dict(draft=0x1000, lens=0x2000, offs=None, nreq=1, rows=2, acc=0x3000, nxt=0x4000,
+             tok=0x5000, cap=8, sl=0x6000, done=None, stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_commit(vp(a["draft"]), vp(a["lens"]), vp(a["offs"]), a["nreq"], a["rows"],
+                          vp(a["acc"]), vp(a["nxt"]), vp(a["tok"]), a["cap"], vp(a["sl"]),
+                          vp(a["done"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(cap=0), 1), (dict(nreq=-1), 1), (dict(nreq=3, rows=2), 1), (dict(draft=None), 1),
+    (dict(lens=None), 1), (dict(acc=None), 1), (dict(nxt=None), 1), (dict(tok=None), 1),
+    (dict(sl=None), 1), (dict(nreq=1025, rows=2000), 1), (dict(cap=1 << 62, nreq=4, rows=4), 1),
+])
+def test_commit_rejects_invalid_arguments(kw, status):
+    assert _commit(**kw) == status
