@@ -250,6 +250,33 @@ def main():
     log("timed %d calls: %.3f ms total, %.1f us/call, wall %.3fs" % (
         args.steps, total_ms, ms_per_step * 1e3, wall))
 
+    # The dominant kernel alone: asd_shard_argmax over the whole rows (offset 0,
+    # width V) is the same row kernel with the same grid as the call above,
+    # writing a 16-byte partial per row instead of an 8-byte record.
+    row_only = None
+    if args.shards == 0 and w.blocks == 1 and w.num_requests > 0:
+        parts_full = torch.empty((w.rows_per_call, 4), dtype=torch.int32, device=dev)
+        for _ in range(3):
+            asd.asd_shard_argmax(logits, 0, w.vocab, draft, out_partials=parts_full)
+        r0 = torch.cuda.Event(enable_timing=True)
+        r1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        r0.record(stream)
+        for _ in range(args.steps):
+            asd.asd_shard_argmax(logits, 0, w.vocab, draft, out_partials=parts_full)
+        r1.record(stream)
+        torch.cuda.synchronize()
+        row_ms = r0.elapsed_time(r1) / args.steps
+        row_bytes = w.logit_bytes_per_call + 4 * w.rows_per_call
+        row_only = {"kernel": "asd_row_kernel (one workgroup per row tile, as in the call)",
+                    "avg_launch_ms": row_ms,
+                    "algorithmic_bytes_per_launch": row_bytes,
+                    "achieved": row_bytes / (row_ms / 1e3) / 1e9,
+                    "frac": row_bytes / (row_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                    "note": "timed with HIP events around asd_shard_argmax(offset 0, width V), "
+                            "the verifier's row pass alone"}
+        log("row kernel alone: %.1f us, %.0f GB/s" % (row_ms * 1e3, row_only["achieved"]))
+
     # Context: torch's own full reduction over the same logits (a read-only pass).
     pe0 = torch.cuda.Event(enable_timing=True)
     pe1 = torch.cuda.Event(enable_timing=True)
@@ -368,6 +395,7 @@ def main():
                      "avg_launch_ms": ms_per_step,
                      "timing": "HIP events on the kernels' stream around the timed calls; "
                                "a call is the row kernel plus the scan kernel"},
+        "row_kernel_roofline": row_only,
         "torch_amax_same_logits_GBps": probe_gbps,
         "kernel_source_sha256_16": kernel_source_hash(),
     }
