@@ -101,6 +101,9 @@ def main():
                     help="bound on the CPU-oracle baseline's timed work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--lmhead", type=int, default=0, metavar="D",
+                    help="LM-head-fused verification: hidden states [rows, D] and output weights "
+                         "[V, D] (bf16) instead of logits; also times the unfused path")
     ap.add_argument("--graph", action="store_true",
                     help="a step is every call of the workload followed by its commit "
                          "(asd_commit), captured once as a HIP graph and replayed")
@@ -126,6 +129,9 @@ def main():
 
     import paper_2608_03447_amd as asd
     import workloads as W
+
+    if args.lmhead:
+        return bench_lmhead(args, torch, asd, W)
 
     dev = torch.device("cuda:0")
     t0 = time.time()
@@ -401,6 +407,88 @@ def main():
     }
     if cpu is not None:
         out["cpu_baseline"] = cpu
+    print(json.dumps(out), flush=True)
+
+
+def bench_lmhead(args, torch, asd, W):
+    """LM-head-fused verification on the workload's rows: z = H W^T on the matrix
+    cores, reduced in the epilogue, never written.  Compared with the unfused
+    path (a library GEMM writing bf16 logits, then asd_verify)."""
+    dev = torch.device("cuda:0")
+    w = W.make_config(args.config)
+    d = args.lmhead
+    rows, V = w.rows_per_call, w.vocab
+    g = torch.Generator(device=dev).manual_seed(1234)
+    hidden = torch.randn((rows, d), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    weight = (torch.randn((V, d), generator=g, device=dev, dtype=torch.float32) * d ** -0.5).to(
+        torch.bfloat16)
+    draft = torch.from_numpy(w.draft_tokens).to(dev)
+    lens = torch.from_numpy(w.block_lens).to(dev)
+    tau = torch.from_numpy(w.tau).to(dev)
+    cap = torch.from_numpy(w.exc_cap).to(dev)
+    budget = torch.from_numpy(w.budget.copy()).to(dev)
+    amax = torch.empty(rows, dtype=torch.int32, device=dev)
+    log("lmhead: %d rows x d %d x V %d (%.2f TFLOP per call)" % (rows, d, V, 2.0 * rows * V * d / 1e12))
+
+    def fused():
+        asd.asd_lmhead_verify(hidden, weight, draft, lens, tau, cap, budget, out_argmax=amax)
+
+    logits = torch.empty((rows, V), dtype=torch.bfloat16, device=dev)
+
+    def unfused():
+        torch.nn.functional.linear(hidden, weight, out=logits)
+        asd.asd_verify(logits, draft, lens, tau, cap, budget)
+
+    def timed(fn):
+        for _ in range(max(args.warmup, 2)):
+            fn()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    fused()
+    torch.cuda.synchronize()
+    fused_ms = timed(fused)
+    unfused_ms = timed(unfused)
+    log("fused %.3f ms, unfused (library GEMM + logits + asd_verify) %.3f ms" % (fused_ms, unfused_ms))
+
+    # Check a sample of rows against exact logits on the host: the argmax must
+    # agree wherever the top-two gap exceeds the rounding bound.
+    import numpy as np
+    fused()
+    torch.cuda.synchronize()
+    sample = np.linspace(0, rows - 1, 16).astype(np.int64)
+    h64 = hidden[torch.from_numpy(sample).to(dev)].float().cpu().numpy().astype(np.float64)
+    w64 = weight.float().cpu().numpy().astype(np.float64)
+    z = h64 @ w64.T
+    bound = 2.0 * d * 2.0 ** -24 * (np.abs(h64) @ np.abs(w64).T).max(axis=1)
+    order = np.argsort(-z, axis=1, kind="stable")
+    gap = z[np.arange(16), order[:, 0]] - z[np.arange(16), order[:, 1]]
+    got = amax.cpu().numpy()[sample]
+    decided = gap > 2 * bound
+    ok = bool(np.all(got[decided] == order[decided, 0]) and
+              np.all(z.max(axis=1) - z[np.arange(16), got] <= 2 * bound))
+    flops = 2.0 * rows * V * d
+    out = {
+        "metric": "verified logit rows/s, LM-head-fused (%s, d=%d)" % (w.name, d),
+        "value": rows / (fused_ms / 1e3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": fused_ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded torch randn hidden states and output weights)",
+        "config": {"workload": "asd_lmhead_verify on %d rows x d %d x V %d bf16" % (rows, d, V),
+                   "rows_per_call": rows, "vocab": V, "hidden": d},
+        "parity": "sampled rows within the rounding bound" if ok else "MISMATCH",
+        "unfused_ms_per_step": unfused_ms,
+        "roofline": {"bound": "mfma", "achieved": flops / (fused_ms / 1e3) / 1e12,
+                     "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": flops / (fused_ms / 1e3) / 1e12 / 2500.0, "traffic": None},
+    }
     print(json.dumps(out), flush=True)
 
 

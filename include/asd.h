@@ -250,6 +250,32 @@ asd_status asd_commit(const int32_t *draft_tokens, const int32_t *block_lens,
                       const int32_t *accept_len, const int32_t *next_token, int32_t *tokens,
                       int64_t capacity, int64_t *seq_len, int32_t *out_committed, void *stream);
 
+/*
+ * asd_lmhead_verify -- asd_verify with the target's output layer fused in: the
+ * logit rows z = H W^T are computed on the matrix cores and reduced at once to
+ * each row's greatest logit, its column and the draft token's logit, the only
+ * values the verifier needs (Sec. 3.3), so the total_rows x V logits are never
+ * written to memory.
+ *
+ * hidden          bf16 [total_rows, d], row-major: the final hidden state of
+ *                 every logit row (teacher-forced rows, Sec. 3.1, Eq. 1).
+ * weight          bf16 [vocab, d], row-major: the output (LM-head) weights.
+ * d               hidden size, a multiple of 64, 64 <= d <= 2^24.  Both base
+ *                 addresses 16-byte aligned.
+ * Logits are binary32 sums of the bf16 products (accumulated on the matrix
+ * cores in an order of their own); a greatest logit of zero is taken as +0.
+ * The other arguments and all outputs are those of asd_verify.  Uses the
+ * library workspace of (device, stream) like asd_verify (allocated on first
+ * use, never during stream capture).
+ */
+asd_status asd_lmhead_verify(const void *hidden, const void *weight, int64_t d, int64_t vocab,
+                             int32_t num_requests, int64_t total_rows,
+                             const int32_t *draft_tokens, const int32_t *block_lens,
+                             const int64_t *row_offsets, const float *tau,
+                             const int32_t *exc_cap, asd_budget *budget_inout,
+                             int32_t *out_accept_len, int32_t *out_next_token,
+                             int32_t *out_argmax, float *out_regret, void *stream);
+
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 

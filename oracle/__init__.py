@@ -166,3 +166,22 @@ def commit(draft_tokens, block_lens, accept_len, next_token, tokens, seq_len, ro
     _load().oracle_commit(_ptr(draft), _ptr(lens), _ptr(offs), lens.shape[0], draft.shape[0],
                           _ptr(acc), _ptr(nxt), _ptr(tok), tok.shape[1], _ptr(sl), _ptr(done))
     return tok, sl, done
+
+
+def lmhead_logits(hidden_bits, weight_bits):
+    """Logit rows z = H W^T of bf16 hidden states [R, d] and output weights [V, d]
+    (uint16 bit patterns): the sum of the bf16 products taken in binary64 (a
+    library matmul), rounded to binary32; a zero sum is +0.  Exact whenever the
+    sum and its partial sums are representable in binary32 (small dyadic inputs)."""
+    def widen(bits):
+        return (np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(
+            np.float32).astype(np.float64)
+    z = widen(hidden_bits) @ widen(weight_bits).T
+    return z.astype(np.float32) + np.float32(0.0)
+
+
+def lmhead_verify(hidden_bits, weight_bits, draft_tokens, block_lens, tau, exc_cap, budget,
+                  row_offsets=None):
+    """The verifier on the logit rows of :func:`lmhead_logits`."""
+    return verify(lmhead_logits(hidden_bits, weight_bits), draft_tokens, block_lens, tau,
+                  exc_cap, budget, row_offsets)

@@ -14,7 +14,7 @@ import torch
 from .build import LIBRARY
 
 __all__ = ["asd_verify", "asd_verify_ws", "asd_shard_argmax", "asd_verify_partials",
-           "asd_opportunity", "asd_commit",
+           "asd_opportunity", "asd_commit", "asd_lmhead_verify",
            "asd_workspace_bytes", "asd_status_string", "asd_version", "asd_release", "AsdError",
            "ASD_F32", "ASD_BF16", "library_path"]
 
@@ -57,6 +57,9 @@ def _load():
     lib.asd_opportunity.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, i32, vp, i32, vp, vp,
                                      vp]
     lib.asd_opportunity.restype = ctypes.c_int
+    lib.asd_lmhead_verify.argtypes = [vp, vp, i64, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp,
+                                      vp, vp, vp]
+    lib.asd_lmhead_verify.restype = ctypes.c_int
     lib.asd_commit.argtypes = [vp, vp, vp, i32, i64, vp, vp, vp, i64, vp, vp, vp]
     lib.asd_commit.restype = ctypes.c_int
     lib.asd_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i64]
@@ -337,3 +340,29 @@ def asd_commit(draft_tokens, block_lens, accept_len, next_token, tokens, seq_len
                                 ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
     if st != 0:
         raise AsdError(st, "asd_commit")
+
+
+def asd_lmhead_verify(hidden, weight, draft_tokens, block_lens, tau, exc_cap, budget, *,
+                      row_offsets=None, out_accept_len=None, out_next_token=None,
+                      out_argmax=None, out_regret=None):
+    """LM-head-fused verification (``asd_lmhead_verify`` of ``include/asd.h``).
+
+    hidden  bf16 [total_rows, d]; weight bf16 [V, d]; other arguments as for :func:`asd_verify`.
+    """
+    for t, name in ((hidden, "hidden"), (weight, "weight")):
+        if t.dim() != 2 or t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous 2-D bfloat16 GPU tensor" % name)
+    if hidden.shape[1] != weight.shape[1] or hidden.device != weight.device:
+        raise ValueError("hidden and weight must share d and device")
+    dev = hidden.device
+    with torch.cuda.device(dev):
+        args, acc, nxt, keep = _marshal(dev, hidden.shape[0], draft_tokens, block_lens, tau,
+                                        exc_cap, budget, row_offsets, out_accept_len,
+                                        out_next_token, out_argmax, out_regret)
+        st = _load().asd_lmhead_verify(ctypes.c_void_p(hidden.data_ptr()),
+                                       ctypes.c_void_p(weight.data_ptr()), hidden.shape[1],
+                                       weight.shape[0], *args)
+    del keep
+    if st != 0:
+        raise AsdError(st, "asd_lmhead_verify")
+    return acc, nxt

@@ -349,6 +349,44 @@ asd_status asd_commit(const int32_t* draft_tokens, const int32_t* block_lens,
                : ASD_EHIP;
 }
 
+asd_status asd_lmhead_verify(const void* hidden, const void* weight, int64_t d, int64_t vocab,
+                             int32_t num_requests, int64_t total_rows,
+                             const int32_t* draft_tokens, const int32_t* block_lens,
+                             const int64_t* row_offsets, const float* tau,
+                             const int32_t* exc_cap, asd_budget* budget_inout,
+                             int32_t* out_accept_len, int32_t* out_next_token,
+                             int32_t* out_argmax, float* out_regret, void* stream) {
+    asd_status st = check_args(hidden, ASD_BF16, vocab, num_requests, total_rows, draft_tokens,
+                               block_lens, tau, exc_cap, budget_inout, out_accept_len,
+                               out_next_token);
+    if (st != ASD_OK || num_requests == 0) return st;
+    if (!weight || d < 64 || d % 64 != 0 || d > ((int64_t)1 << 24)) return ASD_EINVAL;
+    if (((uintptr_t)hidden & 15) != 0 || ((uintptr_t)weight & 15) != 0) return ASD_EINVAL;
+    const int64_t tiles = ((total_rows + 127) / 128) * ((vocab + 127) / 128);
+    if (tiles >= ((int64_t)1 << 31) - 8) return ASD_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = nullptr;
+    if ((st = library_workspace(s, lmhead_workspace_bytes(total_rows, num_requests), &ws)) !=
+        ASD_OK)
+        return st;
+    CallArgs a{};
+    a.logits = nullptr;
+    a.num_requests = num_requests;
+    a.draft_tokens = draft_tokens;
+    a.block_lens = block_lens;
+    a.row_offsets = row_offsets;
+    a.tau = tau;
+    a.exc_cap = exc_cap;
+    a.budget = reinterpret_cast<float2*>(budget_inout);
+    a.out_accept_len = out_accept_len;
+    a.out_next_token = out_next_token;
+    a.out_argmax = out_argmax;
+    a.out_regret = out_regret;
+    return launch_lmhead_verify(hidden, weight, d, vocab, total_rows, a, ws, s) == hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
 const char* asd_status_string(asd_status status) {
     switch (status) {
         case ASD_OK: return "ASD_OK";

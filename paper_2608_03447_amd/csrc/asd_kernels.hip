@@ -457,6 +457,8 @@ struct ScanArgs {
     const RowRecord* records;    // splits == 1 and no shards
     const TilePartial* partials; // split rows: [row][split]; shards: [shard][row]
     int64_t shard_vocab;         // > 0: partials come from vocabulary shards of this width
+    const unsigned long long* row_best;   // LM-head pass: each row's greatest (key, column)
+    const uint32_t* row_draft_bits;       // LM-head pass: each row's draft logit
     int32_t* out_accept_len;
     int32_t* out_next_token;
     float* out_regret;
@@ -468,6 +470,13 @@ __device__ __forceinline__ void combine_row(const ScanArgs& A, int64_t row, int3
                                             unsigned long long& packed, uint32_t& bits,
                                             uint32_t& draft_bits) {
     const bool x_valid = x >= 0 && (int64_t)x < A.vocab;
+    if (A.row_best) {                    // LM-head pass: value bits from the exact key
+        packed = A.row_best[row];
+        const int32_t key = packed_key(packed);
+        bits = key >= 0 ? (uint32_t)key : (0x80000000u | (uint32_t)(-(int64_t)key));
+        draft_bits = x_valid ? A.row_draft_bits[row] : 0u;
+        return;
+    }
     const TilePartial* parts;
     int64_t stride;
     int owner = -1;
@@ -565,7 +574,7 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         float r = 0.0f;
         if (have) {
             const int64_t row = o + p;
-            if (A.partials == nullptr) {
+            if (A.records != nullptr) {
                 const RowRecord rec = A.records[row];
                 y = rec.y_flags & kArgmaxMask;
                 mism = (rec.y_flags & kMismatchBit) != 0u;
@@ -806,6 +815,146 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
     }
 }
 
+// ------------------------------------------- LM-head-fused row pass (MFMA)
+
+// z = H W^T for hidden states H [M, K] and output weights W [N, K] (both bf16,
+// K-contiguous), in binary32 on v_mfma_f32_32x32x16_bf16, reduced at once to
+// each row's greatest (key, column) and the draft token's logit: the R x V
+// logits are never written.
+//
+// Workgroup tile 128 x 128, K step 64; four wavefronts in 2 x 2, each 64 x 64
+// as 2 x 2 MFMA tiles of 32 x 32.  MFMA operand layout (lane l, element e):
+// A row l % 32, k = 8 (l / 32) + e; B column l % 32, same k; accumulator v of
+// lane l is row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32.
+constexpr int kLmTile = 128;
+constexpr int kLmK = 64;
+constexpr int kLmRow = kLmK + 8;     // LDS row stride in bf16 (padded, 144 bytes)
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ void lm_load_tile(const unsigned char* base, int64_t row0,
+                                             int64_t nrows, int64_t K, int64_t k0, int tid,
+                                             u32x4 (&regs)[4]) {
+    // 128 rows x 64 bf16 = 1024 chunks of 16 bytes; thread t takes chunks t + 256 u.
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int c = tid + u * kRowThreads;
+        const int64_t row = row0 + (c >> 3);
+        regs[u] = (u32x4)(0u);
+        if (row < nrows)
+            regs[u] = *(const u32x4*)(base + (row * K + k0 + (c & 7) * 8) * 2);
+    }
+}
+
+__device__ __forceinline__ void lm_store_tile(__bf16* lds, int tid, const u32x4 (&regs)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int c = tid + u * kRowThreads;
+        *(u32x4*)(lds + (c >> 3) * kLmRow + (c & 7) * 8) = regs[u];
+    }
+}
+
+__global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
+    const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ weight,
+    int64_t M, int64_t N, int64_t K, int64_t tiles_m, int64_t tiles,
+    const int32_t* __restrict__ draft_tokens, unsigned long long* __restrict__ row_best,
+    uint32_t* __restrict__ row_draft_bits) {
+    __shared__ __attribute__((aligned(16))) __bf16 As[kLmTile * kLmRow];
+    __shared__ __attribute__((aligned(16))) __bf16 Bs[kLmTile * kLmRow];
+    __shared__ unsigned long long s_best[kLmTile];
+    __shared__ int32_t s_draft[kLmTile];
+
+    // XCD-aware order: workgroup i runs on XCD i % 8; give each XCD a run of
+    // consecutive tiles, M fastest, so one weight tile serves all row tiles
+    // from that XCD's L2.
+    const int64_t per_xcd = gridDim.x / 8;
+    const int64_t linear = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (linear >= tiles) return;
+    const int64_t tm = linear % tiles_m, tn = linear / tiles_m;
+    const int64_t row0 = tm * kLmTile, col0 = tn * kLmTile;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    if (tid < kLmTile) {
+        s_best[tid] = 0ull;
+        s_draft[tid] = row0 + tid < M ? draft_tokens[row0 + tid] : -1;
+    }
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16)(0.0f);
+
+    u32x4 ra[4], rb[4];
+    lm_load_tile(hidden, row0, M, K, 0, tid, ra);
+    lm_load_tile(weight, col0, N, K, 0, tid, rb);
+    for (int64_t k0 = 0; k0 < K; k0 += kLmK) {
+        __syncthreads();                    // previous step's LDS reads are done
+        lm_store_tile(As, tid, ra);
+        lm_store_tile(Bs, tid, rb);
+        __syncthreads();
+        if (k0 + kLmK < K) {                // next step's loads overlap this step's MFMAs
+            lm_load_tile(hidden, row0, M, K, k0 + kLmK, tid, ra);
+            lm_load_tile(weight, col0, N, K, k0 + kLmK, tid, rb);
+        }
+#pragma unroll
+        for (int kk = 0; kk < kLmK / 16; ++kk) {
+            bf16x8 a[2], b[2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int koff = kk * 16 + 8 * (lane >> 5);
+                a[t] = *(const bf16x8*)(As + (wm * 64 + t * 32 + (lane & 31)) * kLmRow + koff);
+                b[t] = *(const bf16x8*)(Bs + (wn * 64 + t * 32 + (lane & 31)) * kLmRow + koff);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j],
+                                                                         0, 0, 0);
+        }
+    }
+
+    // ---- epilogue: per row, the greatest (key, column) of this tile's columns
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int r = wm * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            unsigned long long best = 0ull;
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int c = wn * 64 + j * 32 + (lane & 31);
+                // Copy the element out first: a bit cast of the vector element
+                // itself read element 0 for every v.
+                const float val = acc[i][j][v];
+                const uint32_t bits = __float_as_uint(val);
+                if (col0 + c < N) {
+                    const unsigned long long pk = pack_kc(f32_key(bits), col0 + c);
+                    best = pk > best ? pk : best;
+                    if ((int64_t)s_draft[r] == col0 + c && row0 + r < M)
+                        row_draft_bits[row0 + r] = bits;
+                }
+            }
+#pragma unroll
+            for (int off = 16; off >= 1; off >>= 1) {   // the 32 lanes sharing this row
+                const unsigned long long o = __shfl_xor(best, off, 64);
+                best = o > best ? o : best;
+            }
+            if ((lane & 31) == 0) atomicMax(&s_best[r], best);
+        }
+    }
+    __syncthreads();
+    if (tid < kLmTile && row0 + tid < M) atomicMax(row_best + row0 + tid, s_best[tid]);
+}
+
+__global__ void asd_fill_u64_kernel(unsigned long long* p, int64_t n, unsigned long long v) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launch
@@ -892,6 +1041,40 @@ hipError_t launch_commit(const int32_t* draft_tokens, const int32_t* block_lens,
         draft_tokens, block_lens, row_offsets, num_requests, total_rows, accept_len, next_token,
         tokens, capacity, seq_len, committed);
     return hipGetLastError();
+}
+
+hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t d,
+                                int64_t vocab, int64_t rows, const CallArgs& a, void* workspace,
+                                hipStream_t stream) {
+    unsigned char* ws = (unsigned char*)workspace;
+    unsigned long long* best = (unsigned long long*)ws;
+    uint32_t* draft_bits = (uint32_t*)(ws + lmhead_draft_offset(rows));
+    asd_fill_u64_kernel<<<(unsigned)((rows + 255) / 256), 256, 0, stream>>>(best, rows, 0ull);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const int64_t tiles_m = (rows + kLmTile - 1) / kLmTile;
+    const int64_t tiles = tiles_m * ((vocab + kLmTile - 1) / kLmTile);
+    const int64_t grid = (tiles + 7) / 8 * 8;
+    asd_lmhead_kernel<<<(unsigned)grid, kRowThreads, 0, stream>>>(
+        (const unsigned char*)hidden, (const unsigned char*)weight, rows, vocab, d, tiles_m,
+        tiles, a.draft_tokens, best, draft_bits);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    ScanArgs A = scan_args(a, rows, vocab, 2);
+    A.splits = 1;
+    A.chunk_vecs = 0;
+    A.offsets = a.row_offsets;
+    if (!A.offsets && a.num_requests > kWaveOffsetsMaxRequests) {
+        int64_t* packed = (int64_t*)(ws + lmhead_offsets_offset(rows));
+        asd_offsets_kernel<<<1, kRowThreads, 0, stream>>>(a.num_requests, a.block_lens, packed);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+        A.offsets = packed;
+    }
+    A.records = nullptr;
+    A.partials = nullptr;
+    A.shard_vocab = 0;
+    A.row_best = best;
+    A.row_draft_bits = draft_bits;
+    return launch_scan(A, true, stream);
 }
 
 }  // namespace asd

@@ -107,4 +107,20 @@ hipError_t launch_commit(const int32_t* draft_tokens, const int32_t* block_lens,
                          int64_t capacity, int64_t* seq_len, int32_t* committed,
                          hipStream_t stream);
 
+// LM-head-fused verification: workspace = uint64 best [rows], uint32 draft
+// logits [rows] at lmhead_draft_offset(rows), int64 packed offsets
+// [num_requests] at lmhead_offsets_offset(rows).
+inline size_t lmhead_draft_offset(int64_t rows) {
+    return ((size_t)rows * 8 + 255) / 256 * 256;
+}
+inline size_t lmhead_offsets_offset(int64_t rows) {
+    return lmhead_draft_offset(rows) + ((size_t)rows * 4 + 255) / 256 * 256;
+}
+inline size_t lmhead_workspace_bytes(int64_t rows, int32_t num_requests) {
+    return lmhead_offsets_offset(rows) + ((size_t)num_requests * 8 + 255) / 256 * 256;
+}
+hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t d,
+                                int64_t vocab, int64_t rows, const CallArgs& a, void* workspace,
+                                hipStream_t stream);
+
 }  // namespace asd

@@ -399,3 +399,18 @@ def test_budget_reading_keeps_ledger_within_budget_where_the_other_form_fails():
         if found >= 5:
             break
     assert found >= 1
+
+
+def test_lmhead_logits_exact_regime_equals_integer_matmul():
+    rng = np.random.default_rng(21)
+    for d in (64, 512, 5120):
+        h = rng.integers(-2, 3, size=(7, d))
+        w = rng.integers(-2, 3, size=(33, d))
+        z = oracle.lmhead_logits(W.f32_to_bf16(h.astype(np.float32)),
+                                 W.f32_to_bf16(w.astype(np.float32)))
+        assert z.dtype == np.float32
+        assert np.array_equal(z, (h.astype(np.int64) @ w.T).astype(np.float32))
+    # a zero sum is +0 even when every product is -0
+    z = oracle.lmhead_logits(W.f32_to_bf16(np.zeros((1, 4), np.float32)),
+                             W.f32_to_bf16(-np.ones((1, 4), np.float32)))
+    assert z[0, 0] == 0.0 and not np.signbit(z[0, 0])
