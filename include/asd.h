@@ -260,7 +260,7 @@ asd_status asd_commit(const int32_t *draft_tokens, const int32_t *block_lens,
  * hidden          bf16 [total_rows, d], row-major: the final hidden state of
  *                 every logit row (teacher-forced rows, Sec. 3.1, Eq. 1).
  * weight          bf16 [vocab, d], row-major: the output (LM-head) weights.
- * d               hidden size, a multiple of 64, 64 <= d <= 2^24.  Both base
+ * d               hidden size, a multiple of 128, 128 <= d <= 2^20.  Both base
  *                 addresses 16-byte aligned.
  * Logits are binary32 sums of the bf16 products (accumulated on the matrix
  * cores in an order of their own); a greatest logit of zero is taken as +0.

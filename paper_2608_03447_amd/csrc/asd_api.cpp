@@ -360,9 +360,9 @@ asd_status asd_lmhead_verify(const void* hidden, const void* weight, int64_t d, 
                                block_lens, tau, exc_cap, budget_inout, out_accept_len,
                                out_next_token);
     if (st != ASD_OK || num_requests == 0) return st;
-    if (!weight || d < 64 || d % 64 != 0 || d > ((int64_t)1 << 24)) return ASD_EINVAL;
+    if (!weight || d < 128 || d % 128 != 0 || d > ((int64_t)1 << 20)) return ASD_EINVAL;
     if (((uintptr_t)hidden & 15) != 0 || ((uintptr_t)weight & 15) != 0) return ASD_EINVAL;
-    const int64_t tiles = ((total_rows + 127) / 128) * ((vocab + 127) / 128);
+    const int64_t tiles = ((total_rows + 255) / 256) * ((vocab + 255) / 256);
     if (tiles >= ((int64_t)1 << 31) - 8) return ASD_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;

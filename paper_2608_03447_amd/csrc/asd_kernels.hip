@@ -816,43 +816,122 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
 }
 
 // ------------------------------------------- LM-head-fused row pass (MFMA)
-
+//
 // z = H W^T for hidden states H [M, K] and output weights W [N, K] (both bf16,
 // K-contiguous), in binary32 on v_mfma_f32_32x32x16_bf16, reduced at once to
-// each row's greatest (key, column) and the draft token's logit: the R x V
-// logits are never written.
+// each row's greatest (key, column) and the draft token's logit: the M x N
+// logits never reach memory.
 //
-// Workgroup tile 128 x 128, K step 64; four wavefronts in 2 x 2, each 64 x 64
-// as 2 x 2 MFMA tiles of 32 x 32.  MFMA operand layout (lane l, element e):
-// A row l % 32, k = 8 (l / 32) + e; B column l % 32, same k; accumulator v of
-// lane l is row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32.
-constexpr int kLmTile = 128;
+// One workgroup per 256 x 256 output tile; four wavefronts in 2 x 2, each
+// 128 x 128 as 4 x 4 MFMA tiles whose accumulators live in AGPRs.  MFMA
+// operand layout (lane l, element e): A row l % 32, k = 8 (l / 32) + e; B
+// column l % 32, same k; accumulator v of lane l is row 8 (v / 4) + 4 (l / 32)
+// + v % 4, column l % 32.
+//
+// K steps of 64 go through two LDS stages per operand, each [256 rows][128 B].
+// Global -> LDS copies are buffer loads that write LDS directly (no VGPR
+// staging); rows past M or N read as zero from the buffer resource.  The 16-B
+// chunk c of row r is stored at chunk c ^ lm_swz(r), which keeps both the
+// copies and the fragment reads free of bank conflicts.  The two stages are
+// distinct arrays so the compiler can tell that a copy into one stage does not
+// alias the fragment reads from the other.
+//
+// Software pipeline of one wavefront: the fragments of the next k-slice are
+// read while the current slice's 16 MFMAs issue (one LDS read per MFMA), and
+// the barrier that publishes the next stage sits before the last slice's
+// MFMAs, so the next stage's first reads and copies overlap them.
+constexpr int kLmTile = 256;
 constexpr int kLmK = 64;
-constexpr int kLmRow = kLmK + 8;     // LDS row stride in bf16 (padded, 144 bytes)
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+#define ASD_LDS __attribute__((address_space(3)))
 
-__device__ __forceinline__ void lm_load_tile(const unsigned char* base, int64_t row0,
-                                             int64_t nrows, int64_t K, int64_t k0, int tid,
-                                             u32x4 (&regs)[4]) {
-    // 128 rows x 64 bf16 = 1024 chunks of 16 bytes; thread t takes chunks t + 256 u.
+constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data format
+
+__device__ __forceinline__ int lm_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// One stage of one operand: tile rows 0..255, columns [k0b / 2, k0b / 2 + 64).
+// Row r of the tile starts at byte r * K2 of the buffer.  Wavefront w copies
+// the 1-KB blocks w, w + 4, ..., each 8 rows; lane l fills 16-B position l % 8
+// of row l / 8 with k-chunk (l % 8) ^ lm_swz(row).
+__device__ __forceinline__ void lm_copy_stage(rsrc_t rs, int K2, int k0b, int wave, int lane,
+                                              __bf16* lds) {
+    const int c = (lane & 7) ^ (lane >> 3) ^ (wave & 1);   // (lane & 7) ^ lm_swz(row)
+    const int voff = (wave * 8 + (lane >> 3)) * K2 + c * 16;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int c = tid + u * kRowThreads;
-        const int64_t row = row0 + (c >> 3);
-        regs[u] = (u32x4)(0u);
-        if (row < nrows)
-            regs[u] = *(const u32x4*)(base + (row * K + k0 + (c & 7) * 8) * 2);
+    for (int u = 0; u < 8; ++u) {
+        const int blk = u * 4 + wave;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void ASD_LDS*)(lds + blk * 512), 16,
+                                                 voff + u * 32 * K2, k0b, 0, 0);
     }
 }
 
-__device__ __forceinline__ void lm_store_tile(__bf16* lds, int tid, const u32x4 (&regs)[4]) {
+__device__ __forceinline__ void lm_frags(const __bf16* Ar, const __bf16* Br, int p,
+                                         bf16x8 (&a)[4], bf16x8 (&b)[4]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int c = tid + u * kRowThreads;
-        *(u32x4*)(lds + (c >> 3) * kLmRow + (c & 7) * 8) = regs[u];
+    for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(Ar + i * 32 * kLmK + p);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Br + j * 32 * kLmK + p);
+}
+
+__device__ __forceinline__ void lm_mfma16(const bf16x8 (&a)[4], const bf16x8 (&b)[4],
+                                          f32x16 (&acc)[4][4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+}
+
+// Interleave: one MFMA, then one LDS read, eight times, then eight MFMAs; the
+// variant for the stage boundary also spreads the 16 buffer copies.
+#define LM_SCHED_READS()                                                     \
+    do {                                                                     \
+        _Pragma("unroll") for (int t_ = 0; t_ < 8; ++t_) {                   \
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);               \
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);               \
+        }                                                                    \
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
+    } while (0)
+#define LM_SCHED_READS_COPIES()                                              \
+    do {                                                                     \
+        _Pragma("unroll") for (int t_ = 0; t_ < 8; ++t_) {                   \
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);               \
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);               \
+            __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);               \
+        }                                                                    \
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
+    } while (0)
+
+struct LmCtx {
+    rsrc_t rh, rw;
+    int K2, wave, lane, offA, offB, h, sw;
+};
+
+// One K step on stage (Ac, Bc).  Slices 0..2 prefetch the next slice's
+// fragments.  Before slice 3 all wavefronts meet: the next stage (An, Bn) is
+// complete, (Ac, Bc) is no longer read, so the stage after next is copied into
+// it (k0b) and the next stage's first fragments are read.
+__device__ __forceinline__ void lm_step(const LmCtx& x, const __bf16* Ac, const __bf16* Bc,
+                                        const __bf16* An, const __bf16* Bn, int k0b,
+                                        bf16x8 (&fa)[2][4], bf16x8 (&fb)[2][4],
+                                        f32x16 (&acc)[4][4]) {
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk) {
+        lm_frags(Ac + x.offA, Bc + x.offB, ((2 * (kk + 1) + x.h) ^ x.sw) * 8, fa[(kk + 1) & 1],
+                 fb[(kk + 1) & 1]);
+        lm_mfma16(fa[kk & 1], fb[kk & 1], acc);
+        LM_SCHED_READS();
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this lane's copies of (An, Bn)
+    __syncthreads();
+    lm_copy_stage(x.rh, x.K2, k0b, x.wave, x.lane, (__bf16*)Ac);
+    lm_copy_stage(x.rw, x.K2, k0b, x.wave, x.lane, (__bf16*)Bc);
+    lm_frags(An + x.offA, Bn + x.offB, (x.h ^ x.sw) * 8, fa[0], fb[0]);
+    lm_mfma16(fa[1], fb[1], acc);
+    LM_SCHED_READS_COPIES();
 }
 
 __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
@@ -860,94 +939,126 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
     int64_t M, int64_t N, int64_t K, int64_t tiles_m, int64_t tiles,
     const int32_t* __restrict__ draft_tokens, unsigned long long* __restrict__ row_best,
     uint32_t* __restrict__ row_draft_bits) {
-    __shared__ __attribute__((aligned(16))) __bf16 As[kLmTile * kLmRow];
-    __shared__ __attribute__((aligned(16))) __bf16 Bs[kLmTile * kLmRow];
-    __shared__ unsigned long long s_best[kLmTile];
+    __shared__ __attribute__((aligned(1024))) __bf16 A0[kLmTile * kLmK];
+    __shared__ __attribute__((aligned(1024))) __bf16 B0[kLmTile * kLmK];
+    __shared__ __attribute__((aligned(1024))) __bf16 A1[kLmTile * kLmK];
+    __shared__ __attribute__((aligned(1024))) __bf16 B1[kLmTile * kLmK];
     __shared__ int32_t s_draft[kLmTile];
 
-    // XCD-aware order: workgroup i runs on XCD i % 8; give each XCD a run of
-    // consecutive tiles, M fastest, so one weight tile serves all row tiles
-    // from that XCD's L2.
+    // XCD-aware order: workgroup i runs on XCD i % 8; each XCD takes a run of
+    // consecutive tiles, row tiles fastest, so one weight tile is read from
+    // HBM once and serves every row tile from that XCD's L2.
     const int64_t per_xcd = gridDim.x / 8;
     const int64_t linear = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
     if (linear >= tiles) return;
-    const int64_t tm = linear % tiles_m, tn = linear / tiles_m;
-    const int64_t row0 = tm * kLmTile, col0 = tn * kLmTile;
+    const int64_t row0 = (linear % tiles_m) * kLmTile, col0 = (linear / tiles_m) * kLmTile;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    if (tid < kLmTile) {
-        s_best[tid] = 0ull;
-        s_draft[tid] = row0 + tid < M ? draft_tokens[row0 + tid] : -1;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar LDS targets
+    const int wm = wave >> 1, wn = wave & 1, h = lane >> 5;
+    s_draft[tid] = row0 + tid < M ? draft_tokens[row0 + tid] : -1;
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16)(0.0f);
+
+    LmCtx x;
+    x.K2 = (int)(K * 2);
+    x.rh = __builtin_amdgcn_make_buffer_rsrc((void*)(hidden + row0 * x.K2), (short)0,
+                                             (int)(min((int64_t)kLmTile, M - row0) * x.K2),
+                                             kRsrcWord3);
+    x.rw = __builtin_amdgcn_make_buffer_rsrc((void*)(weight + col0 * x.K2), (short)0,
+                                             (int)(min((int64_t)kLmTile, N - col0) * x.K2),
+                                             kRsrcWord3);
+    x.wave = wave;
+    x.lane = lane;
+    x.h = h;
+    x.sw = lm_swz(lane & 31);
+    x.offA = (wm * 128 + (lane & 31)) * kLmK;
+    x.offB = (wn * 128 + (lane & 31)) * kLmK;
+
+    // K / 64 is even.  Copies past the last stage are clamped to it: they
+    // refill a stage that is no longer read, and the fragments read after the
+    // last stage are never used.
+    const int64_t KT = K / kLmK;
+    bf16x8 fa[2][4], fb[2][4];
+    lm_copy_stage(x.rh, x.K2, 0, wave, lane, A0);
+    lm_copy_stage(x.rw, x.K2, 0, wave, lane, B0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    lm_copy_stage(x.rh, x.K2, 2 * kLmK, wave, lane, A1);
+    lm_copy_stage(x.rw, x.K2, 2 * kLmK, wave, lane, B1);
+    lm_frags(A0 + x.offA, B0 + x.offB, (h ^ x.sw) * 8, fa[0], fb[0]);
+    for (int64_t s = 0; s < KT; s += 2) {
+        lm_step(x, A0, B0, A1, B1, (int)(min(s + 2, KT - 1) * 2 * kLmK), fa, fb, acc);
+        lm_step(x, A1, B1, A0, B0, (int)(min(s + 3, KT - 1) * 2 * kLmK), fa, fb, acc);
     }
 
-    f32x16 acc[2][2];
+    // ---- epilogue, through LDS (the stages are free now).  Four passes, one
+    // per 32-row slice i of each wavefront: E0 holds the slice rows of wm = 0,
+    // E1 those of wm = 1, each [32 rows][256 columns] of logit bits, with the
+    // 16-B chunk c of row lr at chunk c ^ ((c >> 4) & 3) ^ 4 (lr & 3) ^
+    // 8 ((lr >> 2) & 1): conflict-free for the stores and for the row scans.
+    // Columns past N are stored as 0xffffffff, the smallest key.  Then four
+    // threads scan each of the 64 rows, 64 columns each in increasing order.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no copy outlives the main loop
+    uint32_t* const E0 = (uint32_t*)A0;
+    uint32_t* const E1 = (uint32_t*)B0;
+    uint32_t* const Ew = wm ? E1 : E0;
+    int wbase[4];
+    uint32_t wmask[4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 4; ++j) {
+        const int col = wn * 128 + j * 32 + (lane & 31);
+        const int cl = col >> 2;
+        wbase[j] = 4 * 256 * h + ((cl ^ ((cl >> 4) & 3) ^ (h << 3)) << 2) + (col & 3);
+        wmask[j] = col0 + col < N ? 0u : 0xffffffffu;
+    }
+    const int rr = tid >> 2, q = tid & 3;                 // scan: slice row, column quarter
+    const int lrr = rr & 31;
+    const uint32_t* const Er = (rr < 32 ? E0 : E1) + lrr * 256;
+    const int xq = q ^ ((lrr & 3) << 2) ^ (((lrr >> 2) & 1) << 3);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16)(0.0f);
-
-    u32x4 ra[4], rb[4];
-    lm_load_tile(hidden, row0, M, K, 0, tid, ra);
-    lm_load_tile(weight, col0, N, K, 0, tid, rb);
-    for (int64_t k0 = 0; k0 < K; k0 += kLmK) {
-        __syncthreads();                    // previous step's LDS reads are done
-        lm_store_tile(As, tid, ra);
-        lm_store_tile(Bs, tid, rb);
+    for (int i = 0; i < 4; ++i) {
         __syncthreads();
-        if (k0 + kLmK < K) {                // next step's loads overlap this step's MFMAs
-            lm_load_tile(hidden, row0, M, K, k0 + kLmK, tid, ra);
-            lm_load_tile(weight, col0, N, K, k0 + kLmK, tid, rb);
-        }
 #pragma unroll
-        for (int kk = 0; kk < kLmK / 16; ++kk) {
-            bf16x8 a[2], b[2];
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                const int koff = kk * 16 + 8 * (lane >> 5);
-                a[t] = *(const bf16x8*)(As + (wm * 64 + t * 32 + (lane & 31)) * kLmRow + koff);
-                b[t] = *(const bf16x8*)(Bs + (wn * 64 + t * 32 + (lane & 31)) * kLmRow + koff);
-            }
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j],
-                                                                         0, 0, 0);
-        }
-    }
-
-    // ---- epilogue: per row, the greatest (key, column) of this tile's columns
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int r = wm * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-            unsigned long long best = 0ull;
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int c = wn * 64 + j * 32 + (lane & 31);
-                // Copy the element out first: a bit cast of the vector element
-                // itself read element 0 for every v.
+            for (int v = 0; v < 16; ++v) {
+                // The element is copied out before its bits are taken: a bit
+                // cast of the vector element itself read element 0 for every v.
                 const float val = acc[i][j][v];
-                const uint32_t bits = __float_as_uint(val);
-                if (col0 + c < N) {
-                    const unsigned long long pk = pack_kc(f32_key(bits), col0 + c);
-                    best = pk > best ? pk : best;
-                    if ((int64_t)s_draft[r] == col0 + c && row0 + r < M)
-                        row_draft_bits[row0 + r] = bits;
+                Ew[(wbase[j] ^ ((v & 3) << 4)) + 256 * (8 * (v >> 2) + (v & 3))] =
+                    __float_as_uint(val) | wmask[j];
+            }
+        __syncthreads();
+        const int r = (rr >> 5) * 128 + i * 32 + lrr;      // tile row
+        int bk = (int)0x80000000, bc = 0;
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            const uint4 f = *(const uint4*)(Er + ((q * 16 + (c ^ xq)) << 2));
+            const uint32_t fv[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int k = f32_key(fv[e]);
+                if (k > bk) {                              // strict: lowest column on ties
+                    bk = k;
+                    bc = c * 4 + e;
                 }
             }
-#pragma unroll
-            for (int off = 16; off >= 1; off >>= 1) {   // the 32 lanes sharing this row
-                const unsigned long long o = __shfl_xor(best, off, 64);
-                best = o > best ? o : best;
-            }
-            if ((lane & 31) == 0) atomicMax(&s_best[r], best);
         }
+        unsigned long long best = pack_kc(bk, col0 + q * 64 + bc);
+        const int64_t xo = (int64_t)s_draft[r] - col0 - q * 64;
+        if (xo >= 0 && xo < 64 && row0 + r < M)
+            row_draft_bits[row0 + r] = Er[((q * 16 + (((int)xo >> 2) ^ xq)) << 2) + ((int)xo & 3)];
+        unsigned long long o = __shfl_xor(best, 1, 64);
+        best = o > best ? o : best;
+        o = __shfl_xor(best, 2, 64);
+        best = o > best ? o : best;
+        if (q == 0 && row0 + r < M) atomicMax(row_best + row0 + r, best);
     }
-    __syncthreads();
-    if (tid < kLmTile && row0 + tid < M) atomicMax(row_best + row0 + tid, s_best[tid]);
 }
 
 __global__ void asd_fill_u64_kernel(unsigned long long* p, int64_t n, unsigned long long v) {
@@ -978,7 +1089,7 @@ hipError_t launch_verify(const Plan& plan, const CallArgs& a, void* workspace,
     A.splits = plan.splits;
     A.chunk_vecs = plan.chunk_vecs;
     A.offsets = a.row_offsets ? a.row_offsets : packed;
-    A.records = records;
+    A.records = plan.splits == 1 ? records : nullptr;   // record mode only when rows are whole
     A.partials = partials;
     A.shard_vocab = 0;
     return launch_scan(A, plan.splits > 1, stream);

@@ -195,3 +195,30 @@ def _commit(**kw):
 ])
 def test_commit_rejects_invalid_arguments(kw, status):
     assert _commit(**kw) == status
+
+
+def _lmhead(**kw):
+    lib = asd._load()
+    a = dict(hidden=0x1000, weight=0x2000, d=256, vocab=100, nreq=1, rows=2, draft=0x3000,
+             lens=0x4000, offs=None, tau=0x5000, cap=0x6000, budget=0x7000, acc=0x8000,
+             nxt=0x9000, amax=None, reg=None, stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_lmhead_verify(vp(a["hidden"]), vp(a["weight"]), a["d"], a["vocab"], a["nreq"],
+                                 a["rows"], vp(a["draft"]), vp(a["lens"]), vp(a["offs"]),
+                                 vp(a["tau"]), vp(a["cap"]), vp(a["budget"]), vp(a["acc"]),
+                                 vp(a["nxt"]), vp(a["amax"]), vp(a["reg"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=64), 1), (dict(d=192), 1), (dict(d=0), 1), (dict(d=(1 << 20) + 128), 1),
+    (dict(weight=None), 1), (dict(hidden=None), 1), (dict(hidden=0x1008), 1),
+    (dict(weight=0x2008), 1), (dict(vocab=0), 1), (dict(nreq=3, rows=2), 1),
+    (dict(draft=None), 1), (dict(budget=None), 1),
+])
+def test_lmhead_rejects_invalid_arguments(kw, status):
+    assert _lmhead(**kw) == status
+
+
+def test_lmhead_empty_batch_is_a_no_op():
+    assert _lmhead(nreq=0, rows=0) == 0

@@ -42,8 +42,9 @@ def _run(hidden, weight, draft, lens, tau, cap, budget, offsets=None):
             "budget": tb.cpu().numpy()}
 
 
-@pytest.mark.parametrize("rows,vocab,d", [(9, 100, 64), (130, 1027, 128), (300, 5000, 256),
-                                          (17, 257, 5120), (1, 1, 64), (260, 3000, 64)])
+@pytest.mark.parametrize("rows,vocab,d", [(9, 100, 128), (130, 1027, 128), (300, 5000, 256),
+                                          (17, 257, 5120), (1, 1, 128), (260, 3000, 384),
+                                          (600, 1300, 640), (257, 513, 128)])
 def test_exact_regime_bit_exact(rows, vocab, d):
     from asd_gpu import describe, mismatches
     rng = np.random.default_rng(rows * 7 + vocab + d)
