@@ -58,10 +58,20 @@ def algorithmic_bytes(w) -> int:
     return rows * w.vocab * w.logits.itemsize + 4 * rows + 32 * w.num_requests
 
 
-def read_traffic(workload_tag: str, source_hash: str):
-    """HBM bytes per call from the committed rocprofv3 counter summary, scaled by
-    the copy-kernel calibration; None when absent or taken on other sources."""
-    path = os.path.join(PROFILE_DIR, "asd_row_kernel_%s_pmc.md" % workload_tag)
+def workload_tag(config: int, w) -> str:
+    """Name of a workload in profile file names, e.g. b256_k16_v151936_bf16."""
+    kdesc = {1: "8", 2: "16", 3: "16", 4: "32", 5: "1to8"}[config]
+    tag = "b%d_k%s_v%d_%s" % (w.num_requests, kdesc, w.vocab, w.dtype)
+    if w.blocks > 1:
+        tag += "_seq%d" % w.blocks
+    return tag
+
+
+def read_traffic(tag: str, source_hash: str, kernel: str = "asd_row_kernel"):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, scaled by the copy-kernel calibration; None when absent or taken on
+    other sources."""
+    path = os.path.join(PROFILE_DIR, "%s_%s_pmc.md" % (kernel, tag))
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -344,10 +354,8 @@ def main():
                              rows_step, w.vocab, w.dtype, len(times), med)}
         log("oracle: %.2fs per call (median of %d), parity %s" % (med, len(times), parity))
 
+    tag = workload_tag(args.config, w)
     kdesc = {1: "8", 2: "16", 3: "16", 4: "32", 5: "1to8"}[args.config]
-    tag = "b%d_k%s_v%d_%s" % (w.num_requests, kdesc, w.vocab, w.dtype)
-    if w.blocks > 1:
-        tag += "_seq%d" % w.blocks
     if args.shards > 0:
         tag += "_shards%d" % args.shards
     if args.opportunity:
@@ -452,11 +460,21 @@ def bench_lmhead(args, torch, asd, W):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / args.steps
 
+    def gemm_only():
+        torch.nn.functional.linear(hidden, weight, out=logits)
+
+    # Alternate the three paths over rounds so clock and thermal drift affect
+    # them alike; report the median of each.
     fused()
     torch.cuda.synchronize()
-    fused_ms = timed(fused)
-    unfused_ms = timed(unfused)
-    log("fused %.3f ms, unfused (library GEMM + logits + asd_verify) %.3f ms" % (fused_ms, unfused_ms))
+    f_ms, u_ms, g_ms = [], [], []
+    for _ in range(3):
+        f_ms.append(timed(fused))
+        u_ms.append(timed(unfused))
+        g_ms.append(timed(gemm_only))
+    fused_ms, unfused_ms, gemm_ms = (sorted(v)[1] for v in (f_ms, u_ms, g_ms))
+    log("fused %.3f ms, unfused (library GEMM + logits + asd_verify) %.3f ms, library GEMM alone "
+        "%.3f ms (medians of 3 alternating rounds)" % (fused_ms, unfused_ms, gemm_ms))
 
     # Check a sample of rows against exact logits on the host: the argmax must
     # agree wherever the top-two gap exceeds the rounding bound.
@@ -484,10 +502,12 @@ def bench_lmhead(args, torch, asd, W):
         "config": {"workload": "asd_lmhead_verify on %d rows x d %d x V %d bf16" % (rows, d, V),
                    "rows_per_call": rows, "vocab": V, "hidden": d},
         "parity": "sampled rows within the rounding bound" if ok else "MISMATCH",
-        "unfused_ms_per_step": unfused_ms,
+        "unfused_ms_per_step": unfused_ms, "library_gemm_ms": gemm_ms,
         "roofline": {"bound": "mfma", "achieved": flops / (fused_ms / 1e3) / 1e12,
                      "peak": 2500.0, "unit": "TFLOP/s",
-                     "frac": flops / (fused_ms / 1e3) / 1e12 / 2500.0, "traffic": None},
+                     "frac": flops / (fused_ms / 1e3) / 1e12 / 2500.0,
+                     "traffic": read_traffic("%s_d%d" % (workload_tag(args.config, w), d),
+                                             kernel_source_hash(), "asd_lmhead_kernel")},
     }
     print(json.dumps(out), flush=True)
 
