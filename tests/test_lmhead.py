@@ -18,7 +18,7 @@ import workloads as W
 pytestmark = pytest.mark.gpu
 
 
-def _run(hidden, weight, draft, lens, tau, cap, budget, offsets=None):
+def _run(hidden, weight, draft, lens, tau, cap, budget, offsets=None, outputs=True):
     import torch
     import paper_2608_03447_amd as asd
     from asd_gpu import device_logits
@@ -33,13 +33,28 @@ def _run(hidden, weight, draft, lens, tau, cap, budget, offsets=None):
         device_logits(hidden, dev), device_logits(weight, dev),
         torch.from_numpy(np.ascontiguousarray(draft, dtype=np.int32)).to(dev),
         torch.from_numpy(np.asarray(lens, np.int32)).to(dev),
-        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.float32(tau), (n,)))).to(dev),
-        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.int32(cap), (n,)))).to(dev),
-        tb, row_offsets=to, out_argmax=amax, out_regret=regret)
+        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.asarray(tau, np.float32), (n,)))).to(dev),
+        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.asarray(cap, np.int32), (n,)))).to(dev),
+        tb, row_offsets=to, out_argmax=amax if outputs else None,
+        out_regret=regret if outputs else None)
     torch.cuda.synchronize()
     return {"accept_len": acc.cpu().numpy(), "next_token": nxt.cpu().numpy(),
             "argmax": amax.cpu().numpy(), "regret": regret.cpu().numpy(),
             "budget": tb.cpu().numpy()}
+
+
+def _exact_inputs(rng, rows, vocab, d):
+    """Dyadic hidden states and weights whose every partial sum is exact in
+    binary32, and drafts that are the greedy token, the runner-up or invalid."""
+    hidden = W.f32_to_bf16(rng.integers(-2, 3, size=(rows, d)).astype(np.float32))
+    weight = W.f32_to_bf16((rng.integers(-2, 3, size=(vocab, d)) / 2.0).astype(np.float32))
+    z = oracle.lmhead_logits(hidden, weight)
+    y = np.argmax(z, axis=1)
+    second = np.argsort(-z, axis=1, kind="stable")[:, min(1, vocab - 1)]
+    draft = np.where(rng.random(rows) < 0.6, y, second).astype(np.int32)
+    draft[rng.random(rows) < 0.05] = -1
+    draft[rng.random(rows) < 0.02] = vocab + 3
+    return hidden, weight, draft
 
 
 @pytest.mark.parametrize("rows,vocab,d", [(9, 100, 128), (130, 1027, 128), (300, 5000, 256),
@@ -90,3 +105,112 @@ def test_realistic_regime_within_rounding_bound():
     assert np.all(z.max(axis=1) - exact_at_gpu <= 2 * bound)
     r_exact = z.max(axis=1)[:-1] - z[np.arange(rows - 1), draft[:-1]]
     assert np.all(np.abs(g["regret"][:-1] - r_exact) <= 4 * bound[:-1])
+
+
+def test_explicit_row_offsets_in_any_order():
+    """Requests listed in an order other than their rows' (explicit offsets)."""
+    from asd_gpu import describe, mismatches
+    rng = np.random.default_rng(31)
+    rows, vocab, d = 260, 700, 256
+    hidden, weight, draft = _exact_inputs(rng, rows, vocab, d)
+    lens, o = [], 0
+    offs = []
+    while o < rows:
+        k = int(min(rows - o - 1, rng.integers(0, 9)))
+        lens.append(k)
+        offs.append(o)
+        o += k + 1
+    perm = rng.permutation(len(lens))
+    lens = np.asarray(lens, np.int32)[perm]
+    offs = np.asarray(offs, np.int64)[perm]
+    n = len(lens)
+    tau = rng.uniform(0.2, 2.0, n).astype(np.float32)
+    cap = rng.integers(0, 4, n).astype(np.int32)
+    budget = np.stack([rng.uniform(0, 6, n), rng.uniform(0, 1, n)], axis=1)
+    print("case lmhead offsets rows %d requests %d" % (rows, n), flush=True)
+    g = _run(hidden, weight, draft, lens, tau, cap, budget, offsets=offs)
+    r = oracle.lmhead_verify(hidden, weight, draft, lens, tau, cap, budget.astype(np.float32),
+                             row_offsets=offs)
+    bad = mismatches(g, r)
+    assert not bad, "differs in %s: %s" % (bad, describe(g, r))
+
+
+def test_many_requests_use_the_offsets_pass():
+    """More than 1,024 requests without offsets: the packed offsets come from a
+    separate pass instead of each scan wavefront."""
+    from asd_gpu import describe, mismatches
+    rng = np.random.default_rng(32)
+    n = 1100
+    lens = rng.integers(0, 3, n).astype(np.int32)
+    rows, vocab, d = int((lens + 1).sum()), 300, 128
+    hidden, weight, draft = _exact_inputs(rng, rows, vocab, d)
+    budget = np.stack([rng.uniform(0, 4, n), np.zeros(n)], axis=1)
+    print("case lmhead many requests rows %d requests %d" % (rows, n), flush=True)
+    g = _run(hidden, weight, draft, lens, 1.0, 2, budget)
+    r = oracle.lmhead_verify(hidden, weight, draft, lens, 1.0, 2, budget)
+    bad = mismatches(g, r)
+    assert not bad, "differs in %s: %s" % (bad, describe(g, r))
+
+
+def test_optional_outputs_may_be_omitted():
+    rng = np.random.default_rng(33)
+    rows, vocab, d = 130, 1027, 128
+    hidden, weight, draft = _exact_inputs(rng, rows, vocab, d)
+    lens = [8] * 14 + [3]
+    budget = np.stack([rng.uniform(0, 6, 15), np.zeros(15)], axis=1)
+    g = _run(hidden, weight, draft, lens, 1.0, 2, budget, outputs=False)
+    r = oracle.lmhead_verify(hidden, weight, draft, lens, 1.0, 2, budget)
+    assert np.array_equal(g["accept_len"], r["accept_len"])
+    assert np.array_equal(g["next_token"], r["next_token"])
+    assert np.array_equal(g["budget"].view(np.uint32), r["budget"].view(np.uint32))
+
+
+def test_graph_capture_replays_match_eager():
+    """The call allocates nothing once the stream's workspace exists, so it can
+    be captured; every replay equals the eager call and the oracle."""
+    import torch
+    import paper_2608_03447_amd as asd
+    from asd_gpu import device_logits
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(34)
+    rows, vocab, d = 300, 5000, 256
+    hidden, weight, draft = _exact_inputs(rng, rows, vocab, d)
+    lens = [9] * 30
+    n = len(lens)
+    budget0 = np.stack([rng.uniform(0, 6, n), np.zeros(n)], axis=1).astype(np.float32)
+    th, tw = device_logits(hidden, dev), device_logits(weight, dev)
+    td = torch.from_numpy(draft).to(dev)
+    tl = torch.from_numpy(np.asarray(lens, np.int32)).to(dev)
+    tt = torch.full((n,), 1.0, dtype=torch.float32, device=dev)
+    tc = torch.full((n,), 2, dtype=torch.int32, device=dev)
+    pristine = torch.from_numpy(budget0).to(dev)
+    tb = pristine.clone()
+    amax = torch.empty(rows, dtype=torch.int32, device=dev)
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):       # eager call: creates this stream's workspace
+        acc, nxt = asd.asd_lmhead_verify(th, tw, td, tl, tt, tc, tb, out_argmax=amax)
+    torch.cuda.synchronize()
+    eager = [x.cpu().numpy().copy() for x in (acc, nxt, tb, amax)]
+    r = oracle.lmhead_verify(hidden, weight, draft, lens, 1.0, 2, budget0)
+    assert np.array_equal(eager[0], r["accept_len"]) and np.array_equal(eager[1], r["next_token"])
+    assert np.array_equal(eager[2].view(np.uint32), r["budget"].view(np.uint32))
+    assert np.array_equal(eager[3], r["argmax"])
+    graph = torch.cuda.CUDAGraph()
+    tb.copy_(pristine)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=side):
+        asd.asd_lmhead_verify(th, tw, td, tl, tt, tc, tb, out_accept_len=acc, out_next_token=nxt,
+                              out_argmax=amax)
+    for replay in range(3):
+        tb.copy_(pristine)
+        acc.fill_(-5)
+        nxt.fill_(-5)
+        amax.fill_(-5)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = [x.cpu().numpy() for x in (acc, nxt, tb, amax)]
+        for a, b in zip(got, eager):
+            assert np.array_equal(a.view(np.uint32) if a.dtype == np.float32 else a,
+                                  b.view(np.uint32) if b.dtype == np.float32 else b), replay
