@@ -89,6 +89,58 @@ def read_traffic(tag: str, source_hash: str, kernel: str = "asd_row_kernel"):
         return None
 
 
+def acceptance_diagnostics(asd, torch, w, calls, lens, tau, cap, pristine):
+    """The paper's acceptance metrics for one pass over the workload: mean
+    accepted length a, the strict-greedy length (first mismatch), accepted
+    exceptions, budget spent and why each block stopped (end of block, the
+    B = 0 dispatch, the gate, the cap or the budget).  The verifier calls run
+    on the device from the pristine ledger with per-row argmax and regret
+    requested; the counting is host-side reporting of their outputs and feeds
+    no result."""
+    import numpy as np
+    dev = pristine.device
+    n = w.rows_per_call
+    budget = pristine.clone()
+    amax = torch.empty(n, dtype=torch.int32, device=dev)
+    reg = torch.empty(n, dtype=torch.float32, device=dev)
+    K = w.block_lens.astype(np.int64)
+    offs = np.concatenate([[0], np.cumsum(np.maximum(K, 0) + 1)[:-1]]).astype(np.int64)
+    t = {"requests": 0, "accepted": 0, "strict": 0, "exceptions": 0, "spent": 0.0}
+    stops = {"end_of_block": 0, "strict_dispatch": 0, "gate": 0, "cap": 0, "budget": 0}
+    for lg, dr, a_out, x_out in calls:
+        before = budget.cpu().numpy().copy()
+        asd.asd_verify(lg, dr, lens, tau, cap, budget, out_accept_len=a_out,
+                       out_next_token=x_out, out_argmax=amax, out_regret=reg)
+        a, y, r = a_out.cpu().numpy(), amax.cpu().numpy(), reg.cpu().numpy()
+        x, after = dr.cpu().numpy(), budget.cpu().numpy()
+        for i in range(w.num_requests):
+            k, o, ai = int(K[i]), int(offs[i]), int(a[i])
+            mism = x[o:o + k] != y[o:o + k]
+            n_acc = int(mism[:ai].sum())
+            t["requests"] += 1
+            t["accepted"] += ai
+            t["strict"] += int(np.argmax(mism)) if mism.any() else k
+            t["exceptions"] += n_acc
+            t["spent"] += float(after[i, 1]) - float(before[i, 1])
+            if ai == k:
+                stops["end_of_block"] += 1
+            elif before[i, 0] == 0:
+                stops["strict_dispatch"] += 1
+            elif not (float(r[o + ai]) <= float(w.tau[i]) * (k - ai)):
+                stops["gate"] += 1
+            elif n_acc + 1 > int(w.exc_cap[i]):
+                stops["cap"] += 1
+            else:
+                stops["budget"] += 1
+    q = max(t["requests"], 1)
+    return {"blocks": t["requests"], "mean_accept_len": t["accepted"] / q,
+            "mean_strict_accept_len": t["strict"] / q,
+            "mean_accepted_exceptions": t["exceptions"] / q,
+            "mean_budget_spent": t["spent"] / q, "stop_reasons": stops,
+            "note": "one pass over the workload from the pristine ledger; counts taken on the "
+                    "host from the calls' per-row argmax and regret"}
+
+
 def copy_calibration(torch, nbytes=1 << 30, reps=10):
     """Plain device copy of a known size (rocprofv3 --pmc calibration run)."""
     dev = torch.device("cuda:0")
@@ -293,6 +345,13 @@ def main():
                             "the verifier's row pass alone"}
         log("row kernel alone: %.1f us, %.0f GB/s" % (row_ms * 1e3, row_only["achieved"]))
 
+    acceptance = None
+    if args.shards == 0 and not args.graph:
+        acceptance = acceptance_diagnostics(asd, torch, w, calls, lens, tau, cap, pristine)
+        log("acceptance: mean a %.2f, strict %.2f, exceptions %.2f, stops %s" % (
+            acceptance["mean_accept_len"], acceptance["mean_strict_accept_len"],
+            acceptance["mean_accepted_exceptions"], acceptance["stop_reasons"]))
+
     # Context: torch's own full reduction over the same logits (a read-only pass).
     pe0 = torch.cuda.Event(enable_timing=True)
     pe1 = torch.cuda.Event(enable_timing=True)
@@ -410,6 +469,7 @@ def main():
                      "timing": "HIP events on the kernels' stream around the timed calls; "
                                "a call is the row kernel plus the scan kernel"},
         "row_kernel_roofline": row_only,
+        "acceptance": acceptance,
         "torch_amax_same_logits_GBps": probe_gbps,
         "kernel_source_sha256_16": kernel_source_hash(),
     }

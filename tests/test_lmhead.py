@@ -33,8 +33,8 @@ def _run(hidden, weight, draft, lens, tau, cap, budget, offsets=None, outputs=Tr
         device_logits(hidden, dev), device_logits(weight, dev),
         torch.from_numpy(np.ascontiguousarray(draft, dtype=np.int32)).to(dev),
         torch.from_numpy(np.asarray(lens, np.int32)).to(dev),
-        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.asarray(tau, np.float32), (n,)))).to(dev),
-        torch.from_numpy(np.ascontiguousarray(np.broadcast_to(np.asarray(cap, np.int32), (n,)))).to(dev),
+        torch.from_numpy(np.array(np.broadcast_to(np.asarray(tau, np.float32), (n,)))).to(dev),
+        torch.from_numpy(np.array(np.broadcast_to(np.asarray(cap, np.int32), (n,)))).to(dev),
         tb, row_offsets=to, out_argmax=amax if outputs else None,
         out_regret=regret if outputs else None)
     torch.cuda.synchronize()

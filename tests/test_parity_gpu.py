@@ -234,12 +234,35 @@ def test_long_blocks_cross_scan_windows():
 
 # ------------------------------------------------- determinism, workspace, streams
 
-def test_repeated_calls_are_bit_identical():
-    w = W.make_config(2, batch=8)
+@pytest.mark.parametrize("cfg,batch", [(2, 8), (5, 40)])
+def test_repeated_calls_are_bit_identical(cfg, batch):
+    """1,000 calls on the same inputs (a split plan and a ragged batch): every
+    output equals the first call's bit for bit, compared on the device."""
+    import paper_2608_03447_amd as asd
+    from asd_gpu import device_logits
+    w = W.make_config(cfg, batch=batch)
     first = gpu_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
-    for _ in range(20):
-        again = gpu_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
-        assert not mismatches(again, first)
+    assert not mismatches(first, oracle_verify(w.logits, w.draft_tokens, w.block_lens, w.tau,
+                                               w.exc_cap, w.budget))
+    dev = torch.device("cuda:0")
+    tl = device_logits(w.logits, dev)
+    td, tk = torch.from_numpy(w.draft_tokens).to(dev), torch.from_numpy(w.block_lens).to(dev)
+    tt, tc = torch.from_numpy(w.tau).to(dev), torch.from_numpy(w.exc_cap).to(dev)
+    pristine = torch.from_numpy(w.budget.copy()).to(dev)
+    ref = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in first.items()}
+    rows = w.rows_per_call
+    amax = torch.empty(rows, dtype=torch.int32, device=dev)
+    regret = torch.empty(rows, dtype=torch.float32, device=dev)
+    tb = pristine.clone()
+    for call in range(1000):
+        tb.copy_(pristine)
+        amax.fill_(-7)
+        regret.fill_(float("nan"))
+        acc, nxt = asd.asd_verify(tl, td, tk, tt, tc, tb, out_argmax=amax, out_regret=regret)
+        assert (torch.equal(acc, ref["accept_len"]) and torch.equal(nxt, ref["next_token"])
+                and torch.equal(amax, ref["argmax"])
+                and torch.equal(tb.view(torch.int32), ref["budget"].view(torch.int32))
+                and torch.equal(regret.view(torch.int32), ref["regret"].view(torch.int32))), call
 
 
 def test_caller_workspace_matches_library_workspace():
