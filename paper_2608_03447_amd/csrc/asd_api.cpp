@@ -19,11 +19,16 @@ size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
 // Tiles the row kernel aims for: at least two rounds of the 8 resident
 // 256-thread workgroups per CU, so that the last round's stragglers are a
 // small share of the stream (measured on MI355X: 4,352 whole rows of 297 KB
-// stream best unsplit; 2,112 rows of 607 KB and 2,784 rows of 253 KB gain
-// 2-5% from splitting; 544 rows gain about 10%).
+// stream best unsplit; 2,112 rows of 607 KB gain 5% from two splits).
 constexpr int kTilesPerCu = 16;
-// Smallest split worth its own workgroup (vectors of 16 bytes = 16 KiB).
-constexpr int64_t kMinChunkVecs = 1024;
+// Smallest split worth its own workgroup, in vectors of 16 bytes.  With at
+// least as many rows as CUs, 64 KiB: smaller tiles cost more in per-workgroup
+// overhead than they recover in balance (544 rows of 297 KB: 4 splits beat 8
+// by 4%, cold).  With fewer rows than CUs the call is bound by latency and
+// more parallel streams win: 16 KiB (9 rows of 128 KB: 7 splits take 5.2 us,
+// whole rows 9.4 us).
+constexpr int64_t kMinChunkVecs = 4096;
+constexpr int64_t kMinChunkVecsFewRows = 1024;
 
 }  // namespace
 
@@ -38,7 +43,7 @@ Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int32_t num_requests
     int64_t splits = 1;
     if (rows > 0) {
         const int64_t want = ((int64_t)num_cus * kTilesPerCu + rows - 1) / rows;
-        const int64_t most = nvec_max / kMinChunkVecs;
+        const int64_t most = nvec_max / (rows < num_cus ? kMinChunkVecsFewRows : kMinChunkVecs);
         splits = want < most ? want : most;
         if (splits > kMaxSplits) splits = kMaxSplits;
         if (splits < 1) splits = 1;
