@@ -30,20 +30,24 @@
 extern "C" {
 #endif
 
-/* Element type of the logits. */
-typedef enum {
+/* Element type of the logits.  A plain 32-bit integer, so that any value a
+ * caller passes is well defined; values other than these return ASD_EDTYPE. */
+typedef int32_t asd_dtype;
+enum {
     ASD_F32 = 0,   /* IEEE binary32 */
     ASD_BF16 = 1   /* bfloat16: the upper 16 bits of a binary32 value */
-} asd_dtype;
+};
 
-typedef enum {
+/* Status of a call (a plain 32-bit integer, like asd_dtype). */
+typedef int32_t asd_status;
+enum {
     ASD_OK = 0,
     ASD_EINVAL = 1,    /* an argument the host can check is invalid; nothing launched */
     ASD_EDTYPE = 2,    /* unknown dtype; nothing launched */
     ASD_ENOMEM = 3,    /* workspace could not be allocated, or too small */
     ASD_EHIP = 4,      /* a HIP runtime call or kernel launch failed */
     ASD_ECAPTURE = 5   /* the library workspace must grow while the stream is captured */
-} asd_status;
+};
 
 /*
  * Per-request regret ledger (B, s) (Sec. 3.2): total budget B and the regret s
