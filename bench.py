@@ -159,7 +159,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--workload", "--config", dest="config", type=int, default=3,
+                    choices=[1, 2, 3, 4, 5],
+                    help="1: one request, 64 sequential blocks, K=8, V=32,000 f32; "
+                         "2: 32 requests, K=16, V=151,936 bf16; 3 (default): 256 requests, K=16, "
+                         "V=151,936 bf16; 4: 64 requests, K=32, V=151,936 f32; 5: 512 requests, "
+                         "K=1..8, V=129,280 bf16")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle baseline's timed work")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -33,7 +33,7 @@ def gpu_counts(draft, amax, regret, vocab, lens, taus, ps, row_offsets=None, rep
 @pytest.mark.parametrize("cfg", [2, 3, 4, 5])
 def test_opportunity_matches_oracle_on_workloads(cfg):
     w = W.make_config(cfg, batch=None if cfg != 3 else 64)
-    print("case opportunity config %d" % cfg, flush=True)
+    print("case opportunity workload %d" % cfg, flush=True)
     g = gpu_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
     counts, m = gpu_counts(w.draft_tokens, g["argmax"], g["regret"], w.vocab, w.block_lens,
                            TAUS, PS)

@@ -388,7 +388,7 @@ def sharded_verify(logits, draft, lens, tau, cap, budget, num_shards, row_offset
 @pytest.mark.parametrize("cfg,shards", [(3, 8), (3, 3), (4, 8), (5, 8), (5, 1), (2, 2)])
 def test_vocabulary_sharded_equals_unsharded(cfg, shards):
     w = W.make_config(cfg, batch=None if cfg != 3 else 64)
-    print("case sharded config %d x %d shards" % (cfg, shards), flush=True)
+    print("case sharded workload %d x %d shards" % (cfg, shards), flush=True)
     g = sharded_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget, shards)
     r = oracle_verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
     bad = mismatches(g, r)

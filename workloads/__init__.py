@@ -203,7 +203,7 @@ def make_config(index: int, seed: Optional[int] = None, *, batch: Optional[int] 
         nrows = blocks * (K + 1)
         logits, draft, peak, runner = _rows(seed, 1, "f32", V, nrows, 1.0, 3.0, (0.7, 0.2),
                                             [K], blocks)
-        return Workload("config1_seq64_k8_v%d_f32" % V, "f32", V, logits, draft, lens,
+        return Workload("seq64_b1_k8_v%d_f32" % V, "f32", V, logits, draft, lens,
                         np.array([1.5], np.float32), np.array([1], np.int32),
                         np.array([[4.0, 0.0]], np.float32), peak, runner, None, blocks)
     if index in (2, 3):
@@ -221,7 +221,7 @@ def make_config(index: int, seed: Optional[int] = None, *, batch: Optional[int] 
             budget = np.zeros((B, 2), np.float32)
             budget[:, 0] = (16.0 * u01(stream_key(seed, index, _S_BUDGET), 0, B)).astype(np.float32)
             cap = 2
-        return Workload("config%d_b%d_k16_v%d_bf16" % (index, B, V), "bf16", V, logits, draft,
+        return Workload("b%d_k16_v%d_bf16" % (B, V), "bf16", V, logits, draft,
                         lens, np.full(B, 2.0, np.float32), np.full(B, cap, np.int32), budget,
                         peak, runner)
     if index == 4:
@@ -235,7 +235,7 @@ def make_config(index: int, seed: Optional[int] = None, *, batch: Optional[int] 
                                             margin_uniform=(0.0, 0.5))
         total = {"asd": 1.0, "asd_b8": 8.0, "strict": 0.0}[variant]
         budget = np.tile(np.array([[total, 0.0]], np.float32), (B, 1))
-        return Workload("config4_b%d_k32_v%d_f32_%s" % (B, V, variant), "f32", V, logits, draft,
+        return Workload("b%d_k32_v%d_f32_%s" % (B, V, variant), "f32", V, logits, draft,
                         lens, np.full(B, 1.0, np.float32), np.full(B, 4, np.int32), budget,
                         peak, runner)
     if index == 5:
@@ -248,7 +248,7 @@ def make_config(index: int, seed: Optional[int] = None, *, batch: Optional[int] 
         tau = (0.5 + 2.5 * u01(stream_key(seed, 5, _S_TAU), 0, B)).astype(np.float32)
         budget = np.zeros((B, 2), np.float32)
         budget[:, 0] = (10.0 * u01(stream_key(seed, 5, _S_BUDGET), 0, B)).astype(np.float32)
-        return Workload("config5_b%d_ragged1to8_v%d_bf16" % (B, V), "bf16", V, logits, draft,
+        return Workload("b%d_ragged1to8_v%d_bf16" % (B, V), "bf16", V, logits, draft,
                         lens, tau, np.ones(B, np.int32), budget, peak, runner)
     raise ValueError("unknown config %r" % index)
 
