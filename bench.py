@@ -176,8 +176,11 @@ def main():
                     help="LM-head-fused verification: hidden states [rows, D] and output weights "
                          "[V, D] (bf16) instead of logits; also times the unfused path")
     ap.add_argument("--graph", action="store_true",
-                    help="a step is every call of the workload followed by its commit "
-                         "(asd_commit), captured once as a HIP graph and replayed")
+                    help="a step is every call of the workload with its commit "
+                         "(asd_verify_commit), captured once as a HIP graph and replayed")
+    ap.add_argument("--separate-commit", action="store_true",
+                    help="with --graph: asd_verify_ws then asd_commit (two calls per round) "
+                         "instead of asd_verify_commit")
     ap.add_argument("--opportunity", action="store_true",
                     help="also accumulate the opportunity statistic (Eq. 4) every step, from "
                          "the per-row argmax and regret the call writes")
@@ -243,9 +246,13 @@ def main():
 
         def eager_step():
             for lg, dr, a, x in calls:
-                asd.asd_verify_ws(lg, dr, lens, tau, cap, budget, ws, out_accept_len=a,
-                                  out_next_token=x)
-                asd.asd_commit(dr, lens, a, x, tokens, seq_len)
+                if args.separate_commit:
+                    asd.asd_verify_ws(lg, dr, lens, tau, cap, budget, ws, out_accept_len=a,
+                                      out_next_token=x)
+                    asd.asd_commit(dr, lens, a, x, tokens, seq_len)
+                else:
+                    asd.asd_verify_commit(lg, dr, lens, tau, cap, budget, tokens, seq_len,
+                                          workspace=ws, out_accept_len=a, out_next_token=x)
 
         graph = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream(dev)
@@ -498,8 +505,11 @@ def main():
                                     % (args.shards, args.shards) if args.shards else "") +
                                    (", per-row argmax/regret written and the Eq. 4 opportunity"
                                     " counts accumulated each step" if args.opportunity else "") +
-                                   (", every call followed by asd_commit, the step captured as"
-                                    " one HIP graph and replayed" if args.graph else "")),
+                                   ((", every call followed by asd_commit (two calls)"
+                                     if args.separate_commit else
+                                     ", every call with its commit (asd_verify_commit)") +
+                                    ", the step captured as one HIP graph and replayed"
+                                    if args.graph else "")),
                    "vocab_shards": args.shards or 1,
                    "calls_per_step": w.blocks,
                    "rows_per_call": w.rows_per_call, "vocab": w.vocab,

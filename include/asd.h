@@ -255,6 +255,35 @@ asd_status asd_commit(const int32_t *draft_tokens, const int32_t *block_lens,
                       int64_t capacity, int64_t *seq_len, int32_t *out_committed, void *stream);
 
 /*
+ * asd_verify_commit -- asd_verify followed, in the same pass, by the commit of
+ * asd_commit (Sec. 3.3): after request i's scan its wavefront writes the
+ * emitted tokens x_1..x_a, y*_{a+1} and advances its committed length, so a
+ * decoding round is one call instead of two.
+ *
+ * The first fifteen arguments are those of asd_verify (here the packed layout,
+ * row_offsets == NULL, has no request limit).  tokens, capacity, seq_len and
+ * out_committed are those of asd_commit, with the same rules: a request
+ * commits nothing when it is not verified, its a_i + 1 tokens do not fit below
+ * capacity, or seq_len_i is negative.
+ * workspace       NULL: the library workspace of (device, stream), allocated on
+ *                 first use and never during stream capture, as for asd_verify.
+ *                 Otherwise caller memory of workspace_bytes >=
+ *                 asd_workspace_bytes(...) bytes, 256-byte aligned, as for
+ *                 asd_verify_ws; the call then allocates nothing.
+ * Returns ASD_EINVAL also for capacity < 1, missing tokens or seq_len, or
+ * num_requests * capacity overflowing int64.
+ */
+asd_status asd_verify_commit(const void *logits, asd_dtype dtype, int64_t vocab,
+                             int32_t num_requests, int64_t total_rows,
+                             const int32_t *draft_tokens, const int32_t *block_lens,
+                             const int64_t *row_offsets, const float *tau,
+                             const int32_t *exc_cap, asd_budget *budget_inout,
+                             int32_t *out_accept_len, int32_t *out_next_token,
+                             int32_t *out_argmax, float *out_regret, int32_t *tokens,
+                             int64_t capacity, int64_t *seq_len, int32_t *out_committed,
+                             void *stream, void *workspace, size_t workspace_bytes);
+
+/*
  * asd_lmhead_verify -- asd_verify with the target's output layer fused in: the
  * logit rows z = H W^T are computed on the matrix cores and reduced at once to
  * each row's greatest logit, its column and the draft token's logit, the only

@@ -14,7 +14,7 @@ import torch
 from .build import LIBRARY
 
 __all__ = ["asd_verify", "asd_verify_ws", "asd_shard_argmax", "asd_verify_partials",
-           "asd_opportunity", "asd_commit", "asd_lmhead_verify",
+           "asd_opportunity", "asd_commit", "asd_verify_commit", "asd_lmhead_verify",
            "asd_workspace_bytes", "asd_status_string", "asd_version", "asd_release", "AsdError",
            "ASD_F32", "ASD_BF16", "library_path"]
 
@@ -61,6 +61,8 @@ def _load():
                                       vp, vp, vp]
     lib.asd_lmhead_verify.restype = ctypes.c_int
     lib.asd_commit.argtypes = [vp, vp, vp, i32, i64, vp, vp, vp, i64, vp, vp, vp]
+    lib.asd_verify_commit.argtypes = common[:-1] + [vp, i64, vp, vp, vp, vp, sz]
+    lib.asd_verify_commit.restype = ctypes.c_int
     lib.asd_commit.restype = ctypes.c_int
     lib.asd_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i64]
     lib.asd_workspace_bytes.restype = sz
@@ -340,6 +342,46 @@ def asd_commit(draft_tokens, block_lens, accept_len, next_token, tokens, seq_len
                                 ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
     if st != 0:
         raise AsdError(st, "asd_commit")
+
+
+def asd_verify_commit(logits, draft_tokens, block_lens, tau, exc_cap, budget, tokens, seq_len, *,
+                      row_offsets=None, out_accept_len=None, out_next_token=None,
+                      out_argmax=None, out_regret=None, out_committed=None, workspace=None):
+    """Verification and commit in one pass (``asd_verify_commit`` of ``include/asd.h``).
+
+    tokens   int32 [num_requests, capacity]; seq_len int64 [num_requests], both updated in
+             place as by :func:`asd_commit`.  workspace: None (library workspace) or a uint8
+             tensor as for :func:`asd_verify_ws`.  Returns (accept_len, next_token).
+    """
+    _check_logits(logits)
+    dev = logits.device
+    n = block_lens.shape[0]
+    if tokens.dtype != torch.int32 or tokens.dim() != 2 or tokens.shape[0] != n \
+            or not tokens.is_contiguous() or tokens.device != dev:
+        raise ValueError("tokens must be a contiguous int32 (%d, capacity) tensor on %s" % (n, dev))
+    if seq_len.dtype != torch.int64 or seq_len.shape != (n,) or not seq_len.is_contiguous() \
+            or seq_len.device != dev:
+        raise ValueError("seq_len must be a contiguous int64 tensor of shape (%d,) on %s" % (n, dev))
+    if out_committed is not None and (out_committed.dtype != torch.int32
+                                      or out_committed.shape != (n,)
+                                      or out_committed.device != dev):
+        raise ValueError("out_committed must be int32 of shape (%d,) on %s" % (n, dev))
+    if workspace is not None and (workspace.dtype != torch.uint8 or not workspace.is_contiguous()
+                                  or workspace.device != dev):
+        raise ValueError("workspace must be a contiguous uint8 tensor on %s" % dev)
+    with torch.cuda.device(dev):
+        args, acc, nxt, keep = _marshal(dev, logits.shape[0], draft_tokens, block_lens, tau,
+                                        exc_cap, budget, row_offsets, out_accept_len,
+                                        out_next_token, out_argmax, out_regret)
+        p = (lambda t: None if t is None else ctypes.c_void_p(t.data_ptr()))
+        st = _load().asd_verify_commit(
+            ctypes.c_void_p(logits.data_ptr()), _DTYPES[logits.dtype], logits.shape[1],
+            *args[:-1], p(tokens), tokens.shape[1], p(seq_len), p(out_committed), args[-1],
+            p(workspace), 0 if workspace is None else workspace.numel())
+    del keep
+    if st != 0:
+        raise AsdError(st, "asd_verify_commit")
+    return acc, nxt
 
 
 def asd_lmhead_verify(hidden, weight, draft_tokens, block_lens, tau, exc_cap, budget, *,

@@ -125,7 +125,8 @@ asd_status enqueue(const void* logits, asd_dtype dtype, int64_t vocab, int32_t n
                    const int64_t* row_offsets, const float* tau, const int32_t* exc_cap,
                    asd_budget* budget, int32_t* out_accept_len, int32_t* out_next_token,
                    int32_t* out_argmax, float* out_regret, hipStream_t stream, const Plan& plan,
-                   void* workspace) {
+                   void* workspace, int32_t* commit_tokens = nullptr, int64_t commit_capacity = 0,
+                   int64_t* commit_seq_len = nullptr, int32_t* commit_done = nullptr) {
     CallArgs a;
     a.logits = logits;
     a.num_requests = num_requests;
@@ -139,6 +140,10 @@ asd_status enqueue(const void* logits, asd_dtype dtype, int64_t vocab, int32_t n
     a.out_next_token = out_next_token;
     a.out_argmax = out_argmax;
     a.out_regret = out_regret;
+    a.commit_tokens = commit_tokens;
+    a.commit_capacity = commit_capacity;
+    a.commit_seq_len = commit_seq_len;
+    a.commit_done = commit_done;
     (void)dtype;
     (void)vocab;
     (void)total_rows;
@@ -352,6 +357,37 @@ asd_status asd_commit(const int32_t* draft_tokens, const int32_t* block_lens,
                          (hipStream_t)stream) == hipSuccess
                ? ASD_OK
                : ASD_EHIP;
+}
+
+asd_status asd_verify_commit(const void* logits, asd_dtype dtype, int64_t vocab,
+                             int32_t num_requests, int64_t total_rows,
+                             const int32_t* draft_tokens, const int32_t* block_lens,
+                             const int64_t* row_offsets, const float* tau,
+                             const int32_t* exc_cap, asd_budget* budget_inout,
+                             int32_t* out_accept_len, int32_t* out_next_token,
+                             int32_t* out_argmax, float* out_regret, int32_t* tokens,
+                             int64_t capacity, int64_t* seq_len, int32_t* out_committed,
+                             void* stream, void* workspace, size_t workspace_bytes) {
+    asd_status st = check_args(logits, dtype, vocab, num_requests, total_rows, draft_tokens,
+                               block_lens, tau, exc_cap, budget_inout, out_accept_len,
+                               out_next_token);
+    if (st != ASD_OK) return st;
+    if (capacity < 1) return ASD_EINVAL;
+    if (num_requests == 0) return ASD_OK;
+    if (!tokens || !seq_len || capacity > INT64_MAX / num_requests) return ASD_EINVAL;
+    if (workspace && ((uintptr_t)workspace & 255) != 0) return ASD_EINVAL;
+    Plan plan;
+    if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = workspace;
+    if (ws) {
+        if (workspace_bytes < plan.ws_bytes) return ASD_ENOMEM;
+    } else if ((st = library_workspace(s, plan.ws_bytes, &ws)) != ASD_OK) {
+        return st;
+    }
+    return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
+                   row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
+                   out_argmax, out_regret, s, plan, ws, tokens, capacity, seq_len, out_committed);
 }
 
 asd_status asd_lmhead_verify(const void* hidden, const void* weight, int64_t d, int64_t vocab,

@@ -459,6 +459,10 @@ struct ScanArgs {
     int64_t shard_vocab;         // > 0: partials come from vocabulary shards of this width
     const unsigned long long* row_best;   // LM-head pass: each row's greatest (key, column)
     const uint32_t* row_draft_bits;       // LM-head pass: each row's draft logit
+    int32_t* commit_tokens;               // commit in the same pass, or nullptr
+    int64_t commit_capacity;
+    int64_t* commit_seq_len;
+    int32_t* commit_done;
     int32_t* out_accept_len;
     int32_t* out_next_token;
     float* out_regret;
@@ -548,10 +552,12 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
         o = part;
     }
+    const int64_t L = A.commit_tokens ? A.commit_seq_len[i] : 0;   // loaded early
     if (!(K >= 0 && o >= 0 && o + (int64_t)K < A.total_rows)) {
         if (lane == 0) {
             A.out_accept_len[i] = 0;
             A.out_next_token[i] = -1;
+            if (A.commit_tokens && A.commit_done) A.commit_done[i] = 0;
         }
         return;
     }
@@ -632,6 +638,19 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         A.out_accept_len[i] = a;
         A.out_next_token[i] = next;
     }
+    if (A.commit_tokens) {
+        // The commit (Sec. 3.3): x_1..x_a then y*_{a+1} at the request's
+        // committed length, when they fit below capacity.
+        const bool ok = next >= 0 && L >= 0 && L + (int64_t)a + 1 <= A.commit_capacity;
+        if (ok) {
+            int32_t* dst = A.commit_tokens + i * A.commit_capacity + L;
+            for (int64_t j = lane; j <= a; j += 64) dst[j] = j < a ? A.draft_tokens[o + j] : next;
+        }
+        if (lane == 0) {
+            if (ok) A.commit_seq_len[i] = L + (int64_t)a + 1;
+            if (A.commit_done) A.commit_done[i] = ok ? a + 1 : 0;
+        }
+    }
 }
 
 // Packed row offsets for the calls that have no row kernel before the scan.
@@ -658,6 +677,10 @@ ScanArgs scan_args(const CallArgs& a, int64_t rows, int64_t vocab, int elem_byte
     A.out_next_token = a.out_next_token;
     A.out_regret = a.out_regret;
     A.out_argmax = a.out_argmax;
+    A.commit_tokens = a.commit_tokens;
+    A.commit_capacity = a.commit_capacity;
+    A.commit_seq_len = a.commit_seq_len;
+    A.commit_done = a.commit_done;
     return A;
 }
 

@@ -54,18 +54,23 @@ struct Plan {
 
 // Arguments of one verifier call after host validation.
 struct CallArgs {
-    const void* logits;
-    int32_t num_requests;
-    const int32_t* draft_tokens;
-    const int32_t* block_lens;
-    const int64_t* row_offsets;
-    const float* tau;
-    const int32_t* exc_cap;
-    float2* budget;          // (B, s) per request
-    int32_t* out_accept_len;
-    int32_t* out_next_token;
-    int32_t* out_argmax;
-    float* out_regret;
+    const void* logits = nullptr;
+    int32_t num_requests = 0;
+    const int32_t* draft_tokens = nullptr;
+    const int32_t* block_lens = nullptr;
+    const int64_t* row_offsets = nullptr;
+    const float* tau = nullptr;
+    const int32_t* exc_cap = nullptr;
+    float2* budget = nullptr;          // (B, s) per request
+    int32_t* out_accept_len = nullptr;
+    int32_t* out_next_token = nullptr;
+    int32_t* out_argmax = nullptr;
+    float* out_regret = nullptr;
+    // Commit in the same pass (asd_verify_commit); tokens == nullptr: none.
+    int32_t* commit_tokens = nullptr;  // [num_requests][commit_capacity]
+    int64_t commit_capacity = 0;
+    int64_t* commit_seq_len = nullptr; // [num_requests], advanced in place
+    int32_t* commit_done = nullptr;    // [num_requests] or nullptr
 };
 
 Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int32_t num_requests,

@@ -222,3 +222,33 @@ def test_lmhead_rejects_invalid_arguments(kw, status):
 
 def test_lmhead_empty_batch_is_a_no_op():
     assert _lmhead(nreq=0, rows=0) == 0
+
+
+def _verify_commit(**kw):
+    lib = asd._load()
+    a = dict(logits=0x1000, dtype=1, vocab=100, nreq=1, rows=2, draft=0x3000, lens=0x4000,
+             offs=None, tau=0x5000, cap=0x6000, budget=0x7000, acc=0x8000, nxt=0x9000,
+             amax=None, reg=None, tok=0xa000, capacity=8, sl=0xb000, done=None, stream=None,
+             ws=None, ws_bytes=0)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_verify_commit(vp(a["logits"]), a["dtype"], a["vocab"], a["nreq"], a["rows"],
+                                 vp(a["draft"]), vp(a["lens"]), vp(a["offs"]), vp(a["tau"]),
+                                 vp(a["cap"]), vp(a["budget"]), vp(a["acc"]), vp(a["nxt"]),
+                                 vp(a["amax"]), vp(a["reg"]), vp(a["tok"]), a["capacity"],
+                                 vp(a["sl"]), vp(a["done"]), vp(a["stream"]), vp(a["ws"]),
+                                 a["ws_bytes"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(capacity=0), 1), (dict(tok=None), 1), (dict(sl=None), 1),
+    (dict(capacity=1 << 62, nreq=4, rows=4), 1), (dict(ws=0xc010, ws_bytes=1 << 20), 1),
+    (dict(logits=None), 1), (dict(dtype=5), 2), (dict(vocab=0), 1), (dict(nreq=3, rows=2), 1),
+    (dict(draft=None), 1), (dict(budget=None), 1), (dict(logits=0x1001), 1),
+])
+def test_verify_commit_rejects_invalid_arguments(kw, status):
+    assert _verify_commit(**kw) == status
+
+
+def test_verify_commit_empty_batch_is_a_no_op():
+    assert _verify_commit(nreq=0, rows=0) == 0

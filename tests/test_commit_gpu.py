@@ -44,17 +44,105 @@ def test_commit_matches_oracle(cfg):
     assert r_done.min() == 0 and r_done.max() > 1
 
 
-def _rounds(w, blocks, logits, draft, lens, tau, cap, budget, ws, acc, nxt, tokens, seq_len):
+def _rounds(w, blocks, logits, draft, lens, tau, cap, budget, ws, acc, nxt, tokens, seq_len,
+            fused=False):
     n = w.rows_per_call
     for b in range(blocks):
         lg = logits[b * n:(b + 1) * n]
         dr = draft[b * n:(b + 1) * n]
-        asd.asd_verify_ws(lg, dr, lens, tau, cap, budget, ws, out_accept_len=acc[b],
-                          out_next_token=nxt[b])
-        asd.asd_commit(dr, lens, acc[b], nxt[b], tokens, seq_len)
+        if fused:
+            asd.asd_verify_commit(lg, dr, lens, tau, cap, budget, tokens, seq_len, workspace=ws,
+                                  out_accept_len=acc[b], out_next_token=nxt[b])
+        else:
+            asd.asd_verify_ws(lg, dr, lens, tau, cap, budget, ws, out_accept_len=acc[b],
+                              out_next_token=nxt[b])
+            asd.asd_commit(dr, lens, acc[b], nxt[b], tokens, seq_len)
 
 
-def test_graph_captured_rounds_match_eager_and_oracle():
+@pytest.mark.parametrize("cfg,library_ws", [(2, True), (5, True), (5, False)])
+def test_verify_commit_matches_oracle_and_the_two_calls(cfg, library_ws):
+    """asd_verify_commit equals asd_verify then asd_commit, and the oracle's
+    verify then commit, on every output (requests that do not fit included)."""
+    w = W.make_config(cfg, batch=40 if cfg == 2 else 300)
+    rng = np.random.default_rng(10 + cfg)
+    n = w.num_requests
+    cap = 24
+    start = rng.integers(0, 12, n).astype(np.int64)
+    start[::7] = cap - 3
+    start[3] = -1
+    tokens0 = rng.integers(-5, 5, size=(n, cap)).astype(np.int32)
+    logits = t(w.logits.view(np.int16)).view(torch.bfloat16)
+    ws = None
+    if not library_ws:
+        ws = torch.zeros(asd.asd_workspace_bytes(torch.bfloat16, w.vocab, n, w.rows_per_call),
+                         dtype=torch.uint8, device=DEV)
+    budget = t(w.budget.copy())
+    tok, sl = t(tokens0.copy()), t(start.copy())
+    done = torch.empty(n, dtype=torch.int32, device=DEV)
+    amax = torch.empty(w.rows_per_call, dtype=torch.int32, device=DEV)
+    acc, nxt = asd.asd_verify_commit(logits, t(w.draft_tokens), t(w.block_lens), t(w.tau),
+                                     t(w.exc_cap), budget, tok, sl, out_committed=done,
+                                     out_argmax=amax, workspace=ws)
+    # the two calls
+    budget2 = t(w.budget.copy())
+    tok2, sl2 = t(tokens0.copy()), t(start.copy())
+    done2 = torch.empty(n, dtype=torch.int32, device=DEV)
+    acc2, nxt2 = asd.asd_verify(logits, t(w.draft_tokens), t(w.block_lens), t(w.tau),
+                                t(w.exc_cap), budget2)
+    asd.asd_commit(t(w.draft_tokens), t(w.block_lens), acc2, nxt2, tok2, sl2, out_committed=done2)
+    torch.cuda.synchronize()
+    ref = oracle.verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
+    r_tok, r_sl, r_done = oracle.commit(w.draft_tokens, w.block_lens, ref["accept_len"],
+                                        ref["next_token"], tokens0, start)
+    got = [x.cpu().numpy() for x in (acc, nxt, budget, tok, sl, done, amax)]
+    two = [x.cpu().numpy() for x in (acc2, nxt2, budget2, tok2, sl2, done2)]
+    want = [ref["accept_len"], ref["next_token"], ref["budget"], r_tok, r_sl, r_done,
+            ref["argmax"]]
+    for k, (g, r) in enumerate(zip(got, want)):
+        assert np.array_equal(g.view(np.uint32) if g.dtype == np.float32 else g,
+                              r.view(np.uint32) if r.dtype == np.float32 else r), k
+    for k, (g, r) in enumerate(zip(got, two)):
+        assert np.array_equal(g.view(np.uint32) if g.dtype == np.float32 else g,
+                              r.view(np.uint32) if r.dtype == np.float32 else r), k
+    assert r_done.min() == 0 and r_done.max() > 1
+
+
+def test_verify_commit_with_offsets_and_unverified_requests():
+    """Explicit offsets with a gap, a request whose rows do not fit and one with
+    K < 0: those two commit nothing and keep their lengths."""
+    rng = np.random.default_rng(78)
+    vocab, rows = 3000, 120
+    z = rng.normal(0, 2, size=(rows, vocab)).astype(np.float32)
+    y = np.argmax(z, axis=1)
+    draft = np.where(rng.random(rows) < 0.7, y, rng.integers(0, vocab, rows)).astype(np.int32)
+    lens = np.array([8, 0, 5, -1, 8, 3, 12, 8], dtype=np.int32)
+    offs = np.array([0, 10, 12, 20, 30, 117, 100, -4], dtype=np.int64)
+    n = len(lens)
+    budget0 = np.tile(np.array([[3.0, 0.5]], np.float32), (n, 1))
+    tau = np.full(n, 2.0, np.float32)
+    capx = np.full(n, 1, np.int32)
+    capacity = 16
+    start = np.array([0, 3, 15, 2, 4, 0, 1, 0], dtype=np.int64)
+    tokens0 = np.full((n, capacity), -9, np.int32)
+    budget = t(budget0.copy())
+    tok, sl = t(tokens0.copy()), t(start.copy())
+    done = torch.empty(n, dtype=torch.int32, device=DEV)
+    acc, nxt = asd.asd_verify_commit(t(z), t(draft), t(lens), t(tau), t(capx), budget, tok, sl,
+                                     row_offsets=t(offs), out_committed=done)
+    torch.cuda.synchronize()
+    ref = oracle.verify(z, draft, lens, tau, capx, budget0, offs)
+    r_tok, r_sl, r_done = oracle.commit(draft, lens, ref["accept_len"], ref["next_token"],
+                                        tokens0, start, offs)
+    assert np.array_equal(acc.cpu().numpy(), ref["accept_len"])
+    assert np.array_equal(nxt.cpu().numpy(), ref["next_token"])
+    assert np.array_equal(tok.cpu().numpy(), r_tok)
+    assert np.array_equal(sl.cpu().numpy(), r_sl)
+    assert np.array_equal(done.cpu().numpy(), r_done)
+    assert list(r_done[[3, 5, 7]]) == [0, 0, 0]
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_graph_captured_rounds_match_eager_and_oracle(fused):
     blocks = 16
     w = W.make_config(1, batch=blocks)
     logits, draft = t(w.logits), t(w.draft_tokens)
@@ -69,7 +157,7 @@ def test_graph_captured_rounds_match_eager_and_oracle():
     nxt = torch.empty((blocks, 1), dtype=torch.int32, device=DEV)
 
     # eager
-    _rounds(w, blocks, logits, draft, lens, tau, cap, budget, ws, acc, nxt, tokens, seq_len)
+    _rounds(w, blocks, logits, draft, lens, tau, cap, budget, ws, acc, nxt, tokens, seq_len, fused)
     torch.cuda.synchronize()
     eager = [x.cpu().numpy().copy() for x in (budget, tokens, seq_len, acc, nxt)]
 
@@ -97,7 +185,8 @@ def test_graph_captured_rounds_match_eager_and_oracle():
     torch.cuda.current_stream(DEV).wait_stream(side)
     torch.cuda.synchronize()
     with torch.cuda.graph(graph, stream=side):
-        _rounds(w, blocks, logits, draft, lens, tau, cap, budget, ws, acc, nxt, tokens, seq_len)
+        _rounds(w, blocks, logits, draft, lens, tau, cap, budget, ws, acc, nxt, tokens, seq_len,
+                fused)
     for replay in range(3):
         for x, p in zip((budget, tokens, seq_len), pristine):
             x.copy_(p)
