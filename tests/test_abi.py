@@ -252,3 +252,26 @@ def test_verify_commit_rejects_invalid_arguments(kw, status):
 
 def test_verify_commit_empty_batch_is_a_no_op():
     assert _verify_commit(nreq=0, rows=0) == 0
+
+
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_header_compiles_cleanly_as_c_and_cpp(tmp_path, lang):
+    """include/asd.h is a plain C header: it compiles as C99 and C++17 with
+    every warning an error, and a call through it type-checks."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc" if lang == "c" else "g++")
+    if cc is None:
+        pytest.skip("no host compiler")
+    src = tmp_path / ("use.c" if lang == "c" else "use.cpp")
+    src.write_text(
+        '#include "asd.h"\n'
+        "asd_status use(const void *l, const int32_t *d, const int32_t *k, const float *t,\n"
+        "               const int32_t *m, asd_budget *b, int32_t *a, int32_t *x, void *s) {\n"
+        "    return asd_verify(l, ASD_BF16, 100, 1, 2, d, k, 0, t, m, b, a, x, 0, 0, s);\n"
+        "}\n")
+    std = "-std=c99" if lang == "c" else "-std=c++17"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    r = subprocess.run([cc, std, "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", inc, "-c",
+                        str(src), "-o", str(tmp_path / "use.o")], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
