@@ -18,6 +18,10 @@ from .build import LIBRARY, build_oracle
 F32 = 0
 BF16 = 1
 
+RAW_GATE = 1            # flag: gate on r <= g instead of r / q <= g
+ERR_NEGATIVE_K = 1      # error-word bit: some K < 0 (read as 0)
+ERR_ROWS = 2            # error-word bit: some request's rows outside [0, total_rows)
+
 _lib = None
 
 
@@ -34,11 +38,14 @@ def _load():
         lib.oracle_row_argmax.restype = i64
         lib.oracle_argmax_rows.argtypes = [vp, ctypes.c_int, i64, i64, vp]
         lib.oracle_argmax_rows.restype = None
-        lib.oracle_block.argtypes = [i32, vp, vp, vp, vp, vp, f32, vp, f32, i32, vp, vp, vp]
+        lib.oracle_block.argtypes = [i32, vp, vp, vp, vp, vp, f32, vp, f32, i32, ctypes.c_int,
+                                     vp, vp, vp]
         lib.oracle_block.restype = None
         lib.oracle_verify.argtypes = [vp, ctypes.c_int, i64, i32, i64, vp, vp, vp, vp, vp, vp,
                                       vp, vp, vp, vp]
         lib.oracle_verify.restype = ctypes.c_int
+        lib.oracle_verify_ex.argtypes = lib.oracle_verify.argtypes + [ctypes.c_uint32, vp]
+        lib.oracle_verify_ex.restype = ctypes.c_int
         lib.oracle_opportunity.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, i32, vp, i32,
                                            vp, vp]
         lib.oracle_opportunity.restype = None
@@ -75,10 +82,11 @@ def argmax_rows(logits):
     return out
 
 
-def block(x, x_valid, y, z_y, z_x, B, s, g, M):
+def block(x, x_valid, y, z_y, z_x, B, s, g, M, raw_gate=False):
     """Algorithm 1 for one draft block.
 
     ``x`` (K,), ``x_valid`` (K,), ``y`` (K+1,), ``z_y`` (K,), ``z_x`` (K,).
+    ``raw_gate`` gates on r <= g instead of r / q <= g.
     Returns ``(a, next_token, s_new, r)``.
     """
     x = np.ascontiguousarray(x, dtype=np.int32)
@@ -94,17 +102,20 @@ def block(x, x_valid, y, z_y, z_x, B, s, g, M):
     r = np.zeros(max(K, 1), dtype=np.float32)
     _load().oracle_block(K, _ptr(x), _ptr(x_valid), _ptr(y), _ptr(z_y), _ptr(z_x),
                          float(np.float32(B)), _ptr(s_box), float(np.float32(g)), int(M),
-                         _ptr(a), _ptr(nxt), _ptr(r))
+                         int(bool(raw_gate)), _ptr(a), _ptr(nxt), _ptr(r))
     return int(a[0]), int(nxt[0]), np.float32(s_box[0]), r[:K].copy()
 
 
-def verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets=None):
+def verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets=None,
+           raw_gate=False):
     """The whole verifier call on host arrays.
 
     ``budget`` is a float32 [B, 2] array of (total, spent); a new array with the
-    updated ledger is returned (the input is not modified).
+    updated ledger is returned (the input is not modified).  ``raw_gate`` gates
+    on r <= g instead of the paper's r / q <= g.
     Returns a dict with ``accept_len``, ``next_token``, ``budget``, ``argmax``,
-    ``regret`` (rows outside verified requests hold NaN).
+    ``regret`` (rows outside verified requests hold NaN) and ``error`` (the
+    ERR_* bits of the call's requests).
     """
     logits = np.ascontiguousarray(logits)
     code = _dtype_code(logits)
@@ -121,13 +132,15 @@ def verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, row_offsets=N
     nxt = np.zeros(nreq, dtype=np.int32)
     amax = np.zeros(rows, dtype=np.int32)
     regret = np.full(rows, np.nan, dtype=np.float32)
-    rc = _load().oracle_verify(_ptr(logits), code, vocab, nreq, rows, _ptr(draft), _ptr(lens),
-                               _ptr(offs), _ptr(tau), _ptr(cap), _ptr(bud), _ptr(accept),
-                               _ptr(nxt), _ptr(amax), _ptr(regret))
+    err = np.zeros(1, dtype=np.uint32)
+    rc = _load().oracle_verify_ex(_ptr(logits), code, vocab, nreq, rows, _ptr(draft), _ptr(lens),
+                                  _ptr(offs), _ptr(tau), _ptr(cap), _ptr(bud), _ptr(accept),
+                                  _ptr(nxt), _ptr(amax), _ptr(regret),
+                                  RAW_GATE if raw_gate else 0, _ptr(err))
     if rc != 0:
         raise ValueError("oracle_verify rejected its arguments (code %d)" % rc)
     return {"accept_len": accept, "next_token": nxt, "budget": bud, "argmax": amax,
-            "regret": regret}
+            "regret": regret, "error": int(err[0])}
 
 
 def opportunity(draft_tokens, row_argmax, row_regret, vocab, block_lens, taus, ps,
@@ -181,7 +194,7 @@ def lmhead_logits(hidden_bits, weight_bits):
 
 
 def lmhead_verify(hidden_bits, weight_bits, draft_tokens, block_lens, tau, exc_cap, budget,
-                  row_offsets=None):
+                  row_offsets=None, raw_gate=False):
     """The verifier on the logit rows of :func:`lmhead_logits`."""
     return verify(lmhead_logits(hidden_bits, weight_bits), draft_tokens, block_lens, tau,
-                  exc_cap, budget, row_offsets)
+                  exc_cap, budget, row_offsets, raw_gate)

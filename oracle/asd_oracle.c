@@ -29,16 +29,18 @@
  *
  * Readings taken where the paper does not fix a detail (each is listed, with
  * its reason, in the design notes of the repository):
- *   - argmax order: numeric order of the values, with -0 and +0 equal; NaNs
- *     are placed by the IEEE 754-2008 totalOrder predicate (a NaN with the
- *     sign bit clear ranks above +inf, one with it set below -inf, NaNs of one
- *     sign ordered by payload).  Lowest index wins among equal values.
+ *   - argmax order: numeric order of the values, with -0 and +0 equal.  A
+ *     NaN of either sign ranks above +inf and all NaNs rank equal, so the
+ *     first NaN of a row is its argmax (the convention of numpy.argmax).
+ *     Lowest index wins among equal values.
  *   - r_i is one binary32 subtraction of the binary32 values (a bf16 logit is
  *     widened to binary32 exactly first); C_i is a binary32 running sum from
  *     +0 in position order; s' is one binary32 addition s + C_a, and s is left
  *     untouched when no mismatch was accepted.
  *   - gate (Eqs. 7, 11) r_i / q_i <= g is decided as the real-number inequality
- *     r_i <= g * q_i, evaluated in binary64 (exact for q_i < 2^29).
+ *     r_i <= g * q_i, evaluated in binary64 (exact for q_i < 2^29).  A variant
+ *     selected by a flag gates on the raw regret instead, r_i <= g (q_i read
+ *     as 1); the normalized gate is the default.
  *   - budget (Eq. 9) C_t <= B - s is decided as fl32(s + C_t) <= B, which
  *     makes the paper's s' <= B hold exactly after rounding.
  *   - block cap (Eq. 10) N_t <= M.
@@ -48,8 +50,10 @@
  *   - the bonus row's draft entry is ignored.  The per-row regret output is
  *     written for the rows of verified requests only: r_i at draft rows, +0
  *     at the bonus row.
- *   - a request whose rows do not fit in [0, total_rows) or whose K is
- *     negative is not verified: a = 0, next token = -1, state untouched.
+ *   - a negative K is read as K = 0 (the request owns one row, its bonus
+ *     row) and is reported in the error word.  A request whose rows do not
+ *     fit in [0, total_rows) is not verified: a = 0, next token = -1, state
+ *     untouched, also reported in the error word.
  *
  * Parity unpinned: none of the functions below is unpinned; the seeded input
  * generators live elsewhere and are described with the workloads.
@@ -62,6 +66,13 @@
 
 #define ORACLE_F32 0
 #define ORACLE_BF16 1
+
+/* flags of oracle_verify_ex */
+#define ORACLE_RAW_GATE 1u          /* gate on r_i <= g instead of r_i / q_i <= g */
+
+/* bits of the error word of oracle_verify_ex */
+#define ORACLE_ERR_NEGATIVE_K 1u    /* some K_i < 0, read as 0 */
+#define ORACLE_ERR_ROWS 2u          /* some request's rows outside [0, total_rows) */
 
 /* ---------------------------------------------------------------- values */
 
@@ -83,37 +94,18 @@ static float logit_at(const void *logits, int dtype, int64_t vocab,
     return ((const float *)logits)[k];
 }
 
-static uint32_t float_bits(float f)
-{
-    uint32_t u;
-    memcpy(&u, &f, sizeof u);
-    return u;
-}
-
 /*
  * Does value a rank strictly above value b?
- * Non-NaN values: the ordinary IEEE comparison a > b (so -0 and +0 tie).
- * NaNs: IEEE 754-2008 section 5.10 totalOrder -- positive NaNs lie above every
- * number, negative NaNs below every number; two positive NaNs are ordered by
- * payload (larger above), two negative NaNs by payload reversed.
+ * Two numbers: the ordinary IEEE comparison a > b (so -0 and +0 tie).  A NaN
+ * of either sign ranks above every number, and no NaN ranks above another.
  */
 int oracle_ranks_above(float a, float b)
 {
-    int a_nan = isnan(a), b_nan = isnan(b);
-    if (!a_nan && !b_nan)
-        return a > b;
-    if (a_nan && !b_nan)
-        return !signbit(a);
-    if (!a_nan && b_nan)
-        return signbit(b) ? 1 : 0;
-    /* both NaN */
-    if (signbit(a) != signbit(b))
-        return !signbit(a);
-    {
-        uint32_t pa = float_bits(a) & 0x007fffffu;
-        uint32_t pb = float_bits(b) & 0x007fffffu;
-        return signbit(a) ? (pa < pb) : (pa > pb);
-    }
+    if (isnan(b))
+        return 0;
+    if (isnan(a))
+        return 1;
+    return a > b;
 }
 
 /* Eq. 1: y*_i = argmax_v z_i(v); the first (lowest) index among equals. */
@@ -149,12 +141,13 @@ void oracle_argmax_rows(const void *logits, int dtype, int64_t vocab,
  *   z_x[0..K-1]      the target logits z_i(x_i) (not read where x_valid == 0)
  *   B_total, *s      the request state (B, s); *s is updated in place
  *   g, M             the local gate and the per-block exception cap
+ *   raw_gate         nonzero: gate on r_i <= g (q_i read as 1)
  * Outputs: *a (accepted prefix length) and *next (recovery or bonus token);
  * r_out[0..K-1] receives r_i when non-NULL.
  */
 void oracle_block(int32_t K, const int32_t *x, const uint8_t *x_valid,
                   const int32_t *y, const float *z_y, const float *z_x,
-                  float B_total, float *s, float g, int32_t M,
+                  float B_total, float *s, float g, int32_t M, int raw_gate,
                   int32_t *a_out, int32_t *next_out, float *r_out)
 {
     int32_t a;
@@ -183,7 +176,7 @@ void oracle_block(int32_t K, const int32_t *x, const uint8_t *x_valid,
         int64_t N_prev = 0;
 
         for (int32_t i = 0; i < K; ++i)
-            q[i] = K - (i + 1) + 1;                               /* Eq. 6 */
+            q[i] = raw_gate ? 1 : K - (i + 1) + 1;                /* Eq. 6 */
 
         for (int32_t i = 0; i < K; ++i) {                         /* Eq. 8 */
             /* d_i r_i adds nothing at a match (r_i there may be inf/NaN). */
@@ -238,15 +231,18 @@ void oracle_block(int32_t K, const int32_t *x, const uint8_t *x_valid,
  * out_argmax    [total_rows] or NULL: y* of every row
  * out_regret    [total_rows] or NULL: r of every draft row of a verified
  *               request, +0 for its bonus row; other rows are not written
+ * flags         0, or ORACLE_RAW_GATE
+ * error_word    NULL, or ORed with ORACLE_ERR_* for the requests that have them
  * Returns 0, or 1 for an argument the call cannot work with.
  */
-int oracle_verify(const void *logits, int dtype, int64_t vocab,
-                  int32_t num_requests, int64_t total_rows,
-                  const int32_t *draft, const int32_t *block_lens,
-                  const int64_t *row_offsets, const float *tau,
-                  const int32_t *exc_cap, float *budget,
-                  int32_t *out_accept_len, int32_t *out_next_token,
-                  int32_t *out_argmax, float *out_regret)
+int oracle_verify_ex(const void *logits, int dtype, int64_t vocab,
+                     int32_t num_requests, int64_t total_rows,
+                     const int32_t *draft, const int32_t *block_lens,
+                     const int64_t *row_offsets, const float *tau,
+                     const int32_t *exc_cap, float *budget,
+                     int32_t *out_accept_len, int32_t *out_next_token,
+                     int32_t *out_argmax, float *out_regret,
+                     uint32_t flags, uint32_t *error_word)
 {
     int32_t *y_all;
     int64_t packed_offset = 0;
@@ -263,13 +259,17 @@ int oracle_verify(const void *logits, int dtype, int64_t vocab,
     }
 
     for (int32_t i = 0; i < num_requests; ++i) {
-        int32_t K = block_lens[i];
+        int32_t K = block_lens[i] > 0 ? block_lens[i] : 0;
         int64_t o = row_offsets ? row_offsets[i] : packed_offset;
-        packed_offset += (int64_t)(K > 0 ? K : 0) + 1;
+        packed_offset += (int64_t)K + 1;
 
-        if (K < 0 || o < 0 || o + (int64_t)K >= total_rows) {
+        if (block_lens[i] < 0 && error_word)
+            *error_word |= ORACLE_ERR_NEGATIVE_K;
+        if (o < 0 || o + (int64_t)K >= total_rows) {
             out_accept_len[i] = 0;
             out_next_token[i] = -1;
+            if (error_word)
+                *error_word |= ORACLE_ERR_ROWS;
             continue;
         }
 
@@ -292,7 +292,8 @@ int oracle_verify(const void *logits, int dtype, int64_t vocab,
             }
 
             oracle_block(K, x, x_valid, y, z_y, z_x, budget[2 * i], &s,
-                         tau[i], exc_cap[i], &a, &next, r);
+                         tau[i], exc_cap[i], (flags & ORACLE_RAW_GATE) != 0,
+                         &a, &next, r);
 
             budget[2 * i + 1] = s;
             out_accept_len[i] = a;
@@ -314,6 +315,21 @@ int oracle_verify(const void *logits, int dtype, int64_t vocab,
     return 0;
 }
 
+/* oracle_verify_ex with the normalized gate and no error word. */
+int oracle_verify(const void *logits, int dtype, int64_t vocab,
+                  int32_t num_requests, int64_t total_rows,
+                  const int32_t *draft, const int32_t *block_lens,
+                  const int64_t *row_offsets, const float *tau,
+                  const int32_t *exc_cap, float *budget,
+                  int32_t *out_accept_len, int32_t *out_next_token,
+                  int32_t *out_argmax, float *out_regret)
+{
+    return oracle_verify_ex(logits, dtype, vocab, num_requests, total_rows,
+                            draft, block_lens, row_offsets, tau, exc_cap,
+                            budget, out_accept_len, out_next_token,
+                            out_argmax, out_regret, 0u, NULL);
+}
+
 /* -------------------------------------------- opportunity statistic (Eq. 4) */
 
 /*
@@ -325,8 +341,9 @@ int oracle_verify(const void *logits, int dtype, int64_t vocab,
  * (Eq. 5; a draft id outside [0, V) is a mismatch).  A mismatch contributes to
  * (tau, p) when r_i <= tau, i + p <= K, and x_l = y*_l for every l in
  * i+1 .. i+p.  y* and r are the per-row argmax and regret of a verifier call
- * on the same batch (its out_argmax / out_regret).  Requests whose rows do not
- * fit in [0, total_rows), or with K < 0, are not evaluated.
+ * on the same batch (its out_argmax / out_regret).  A negative K is read as 0
+ * (no draft positions); requests whose rows do not fit in [0, total_rows) are
+ * not evaluated.
  */
 void oracle_opportunity(const int32_t *draft, const int32_t *row_argmax,
                         const float *row_regret, int64_t vocab,
@@ -338,10 +355,10 @@ void oracle_opportunity(const int32_t *draft, const int32_t *row_argmax,
 {
     int64_t packed_offset = 0;
     for (int32_t req = 0; req < num_requests; ++req) {
-        int32_t K = block_lens[req];
+        int32_t K = block_lens[req] > 0 ? block_lens[req] : 0;
         int64_t o = row_offsets ? row_offsets[req] : packed_offset;
-        packed_offset += (int64_t)(K > 0 ? K : 0) + 1;
-        if (K < 0 || o < 0 || o + (int64_t)K >= total_rows)
+        packed_offset += (int64_t)K + 1;
+        if (o < 0 || o + (int64_t)K >= total_rows)
             continue;
         for (int32_t i = 1; i <= K; ++i) {
             int64_t row = o + i - 1;
@@ -384,9 +401,10 @@ void oracle_opportunity(const int32_t *draft, const int32_t *row_argmax,
  * tokens     [num_requests][capacity] committed tokens of each request
  * seq_len    [num_requests] committed length, advanced in place by a + 1
  * committed  [num_requests] or NULL: tokens committed this round (a + 1), or 0
- * A request whose rows do not fit in [0, total_rows), with next_token < 0 (not
- * verified), with a outside [0, K], with seq_len < 0, or whose a + 1 tokens do
- * not fit in [seq_len, capacity), commits nothing.
+ * A negative K is read as 0, as the verifier reads it.  A request whose rows
+ * do not fit in [0, total_rows), with next_token < 0 (not verified), with a
+ * outside [0, K], with seq_len < 0, or whose a + 1 tokens do not fit in
+ * [seq_len, capacity), commits nothing.
  */
 void oracle_commit(const int32_t *draft, const int32_t *block_lens,
                    const int64_t *row_offsets, int32_t num_requests,
@@ -397,14 +415,14 @@ void oracle_commit(const int32_t *draft, const int32_t *block_lens,
 {
     int64_t packed_offset = 0;
     for (int32_t i = 0; i < num_requests; ++i) {
-        int32_t K = block_lens[i];
+        int32_t K = block_lens[i] > 0 ? block_lens[i] : 0;
         int64_t o = row_offsets ? row_offsets[i] : packed_offset;
         int32_t a = accept_len[i];
         int64_t L = seq_len[i];
-        packed_offset += (int64_t)(K > 0 ? K : 0) + 1;
+        packed_offset += (int64_t)K + 1;
         if (committed)
             committed[i] = 0;
-        if (K < 0 || o < 0 || o + (int64_t)K >= total_rows)
+        if (o < 0 || o + (int64_t)K >= total_rows)
             continue;                          /* rows of a request asd_verify skips */
         if (next_token[i] < 0 || L < 0 || a < 0 || a > K || L + a + 1 > capacity)
             continue;

@@ -71,3 +71,19 @@ def test_commit_skips_what_does_not_fit():
     tok, sl, done = oracle.commit(draft, lens, acc, np.array([-1, 8], np.int32),
                                   np.zeros((2, 9), np.int32), [0, -3])
     assert done.tolist() == [0, 0] and sl.tolist() == [0, -3]
+
+
+def test_negative_block_length_commits_like_zero():
+    """A negative K is read as 0 by the verifier (one bonus row), so its request
+    emits one token, the argmax of that row, and the commit takes it."""
+    logits = np.zeros((4, 3), dtype=np.float32)
+    logits[0, 2] = 1.0
+    logits[1, 1] = 1.0
+    draft = np.array([2, 0, 1, 0], dtype=np.int32)
+    lens = [-2, 2]
+    out = oracle.verify(logits, draft, lens, [1.0] * 2, [1] * 2, [[0.0, 0.0]] * 2)
+    assert out["accept_len"].tolist() == [0, 0] and out["next_token"].tolist() == [2, 1]
+    tok, sl, done = oracle.commit(draft, lens, out["accept_len"], out["next_token"],
+                                  np.full((2, 4), -1, np.int32), [1, 0])
+    assert tok[0].tolist() == [-1, 2, -1, -1] and sl[0] == 2 and done[0] == 1
+    assert tok[1].tolist() == [1, -1, -1, -1] and sl[1] == 1 and done[1] == 1

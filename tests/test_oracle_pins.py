@@ -7,7 +7,8 @@ Each test checks the oracle against something other than itself:
   * brute force over every prefix and every accepted-mismatch subset, in
     exact rational arithmetic, for the longest feasible prefix (Eqs. 9-12),
   * the paper's invariants (s' <= B after Eq. 13; Proposition 1),
-  * numpy.argmax and a sort-key formulation for the argmax order (Eq. 1).
+  * numpy.argmax for the argmax order (Eq. 1), NaNs included: numpy's argmax
+    returns the first NaN of a row, which is the order the verifier takes.
 """
 import json
 import math
@@ -150,8 +151,9 @@ def _frac(v):
     return Fraction(float(v))
 
 
-def brute_force_block(logits, draft, K, g, M, B, s):
-    """Longest feasible prefix by Eqs. 9-12, two independent ways, exactly."""
+def brute_force_block(logits, draft, K, g, M, B, s, raw_gate=False):
+    """Longest feasible prefix by Eqs. 9-12, two independent ways, exactly.
+    With ``raw_gate`` every mismatch must satisfy r <= g instead of r / q <= g."""
     V = logits.shape[1]
     y = np.argmax(logits, axis=1)
     valid = [(0 <= int(draft[i]) < V) for i in range(K)]
@@ -163,7 +165,7 @@ def brute_force_block(logits, draft, K, g, M, B, s):
     def gate_ok(i):
         if r[i] is None:
             return False
-        q = K - (i + 1) + 1
+        q = 1 if raw_gate else K - (i + 1) + 1
         if math.isinf(g):
             return g > 0
         return r[i] <= _frac(g) * q
@@ -221,6 +223,38 @@ def test_longest_feasible_prefix_brute_force():
         strict_a = strict_greedy(logits, draft, [K])[0][0]
         n_nontrivial += int(a > strict_a)
     assert n_nontrivial > 100          # the brute force exercised accepted mismatches
+
+
+def test_raw_gate_variant_brute_force():
+    """The raw-gate variant (r <= g at every accepted mismatch) against the
+    same two-way brute force; it never accepts more than the paper's gate for
+    g >= 0 (q >= 1), and equals it when every mismatch sits at q = 1."""
+    rng = np.random.default_rng(2609)
+    gates = [-1.0, 0.0, 0.25, 0.5, 1.0, 1.5, np.inf]
+    n_differ = 0
+    for trial in range(1200):
+        K, V = int(rng.integers(0, 9)), int(rng.integers(1, 6))
+        logits = (rng.integers(-8, 9, size=(K + 1, V)) / 4.0).astype(np.float32)
+        y = np.argmax(logits, axis=1)
+        draft = np.where(rng.random(K + 1) < 0.55, y, rng.integers(0, V, K + 1)).astype(np.int32)
+        g = float(rng.choice(gates))
+        M = int(rng.choice([0, 1, 2, 3, 2**31 - 1]))
+        B = float(rng.choice([0.25, 1.0, 2.0, 3.75, np.inf]))
+        raw = oracle.verify(logits, draft, [K], [g], [M], [[B, 0.0]], raw_gate=True)
+        norm = oracle.verify(logits, draft, [K], [g], [M], [[B, 0.0]])
+        a, nxt = brute_force_block(logits, draft, K, g, M, B, 0.0, raw_gate=True)
+        assert raw["accept_len"][0] == a and raw["next_token"][0] == nxt, (trial, K, g, M, B)
+        if g >= 0:
+            assert raw["accept_len"][0] <= norm["accept_len"][0]
+        n_differ += int(raw["accept_len"][0] != norm["accept_len"][0])
+        if K > 0 and np.all(draft[:K - 1] == y[:K - 1]):      # only position K can mismatch
+            assert raw["accept_len"][0] == norm["accept_len"][0]
+    assert n_differ > 50               # the two gates were told apart
+    # B = 0 dispatches to strict greedy under either gate
+    logits = np.array([[0.0, 1.0], [1.0, 0.0], [0.0, 1.0]], dtype=np.float32)
+    draft = np.array([0, 0, 0], dtype=np.int32)
+    out = oracle.verify(logits, draft, [2], [np.inf], [5], [[0.0, 0.0]], raw_gate=True)
+    assert (out["accept_len"][0], out["next_token"][0]) == (0, 1)
 
 
 # --------------------------------------------------------- paper invariants
@@ -305,14 +339,26 @@ def test_out_of_range_draft_is_never_accepted():
         assert out["regret"][1] == np.inf
 
 
-def test_invalid_requests_are_not_verified():
+def test_negative_block_length_reads_as_zero_and_bad_rows_are_not_verified():
     logits = np.zeros((5, 3), dtype=np.float32)
+    logits[2, 1] = 1.0
     draft = np.zeros(5, dtype=np.int32)
     out = oracle.verify(logits, draft, [1, -1, 2], [1.0] * 3, [1] * 3,
                         [[1.0, 0.25]] * 3, row_offsets=[0, 2, 3])
+    # K = -1 is K = 0: the request's one row at o = 2 is its bonus row
     assert list(out["accept_len"]) == [1, 0, 0]
-    assert list(out["next_token"]) == [0, -1, -1]      # row 3 + 2 is past the end
+    assert list(out["next_token"]) == [0, 1, -1]      # row 3 + 2 is past the end
     assert list(out["budget"][:, 1]) == [0.25, 0.25, 0.25]
+    assert out["regret"][2] == 0.0 and not np.signbit(out["regret"][2])
+    assert out["error"] == oracle.ERR_NEGATIVE_K | oracle.ERR_ROWS
+    # the packed layout gives a negative K one row, like K = 0
+    neg = oracle.verify(logits, draft, [1, -7, 1], [1.0] * 3, [1] * 3, [[1.0, 0.25]] * 3)
+    zero = oracle.verify(logits, draft, [1, 0, 1], [1.0] * 3, [1] * 3, [[1.0, 0.25]] * 3)
+    for k in ("accept_len", "next_token", "budget", "argmax"):
+        assert np.array_equal(neg[k], zero[k])
+    assert neg["error"] == oracle.ERR_NEGATIVE_K and zero["error"] == 0
+    ok = oracle.verify(logits, draft, [1, 2], [1.0] * 2, [1] * 2, [[1.0, 0.0]] * 2)
+    assert ok["error"] == 0
 
 
 def test_ledger_carried_across_sessions():
@@ -349,24 +395,27 @@ def test_argmax_matches_numpy_on_finite_values_with_signed_zeros_and_infs():
         assert np.array_equal(oracle.argmax_rows(xb), np.argmax(W.bf16_to_f32(xb), axis=1))
 
 
-def _total_order_key(x):
-    """Sort key of IEEE totalOrder with -0 and +0 merged (independent of the oracle)."""
-    u = x.view(np.uint32).astype(np.int64)
-    mag = u & 0x7FFFFFFF
-    return np.where(u >> 31 == 1, -mag, mag)
-
-
-def test_argmax_nan_placement_follows_total_order():
+def test_argmax_with_nans_matches_numpy_first_nan():
+    """numpy.argmax returns the first NaN of a row (NaN propagates through its
+    maximum); the verifier's order ranks every NaN, of either sign and any
+    payload, above +inf and all NaNs equal, so the two must agree everywhere."""
     rng = np.random.default_rng(4)
     specials = np.array([0x7FC00000, 0x7F800001, 0x7FFFFFFF, 0xFFC00000, 0xFF800001,
-                         0x7F800000, 0xFF800000, 0x80000000, 0x00000000, 0x3F800000],
-                        dtype=np.uint32).view(np.float32)
-    for _ in range(300):
-        V = int(rng.integers(1, 40))
-        x = rng.choice(specials, size=(1, V)).astype(np.float32)
-        key = _total_order_key(x[0])
-        expect = int(np.flatnonzero(key == key.max())[0])
-        assert oracle.argmax_rows(x)[0] == expect
+                         0xFFFFFFFF, 0x7F800000, 0xFF800000, 0x80000000, 0x00000000,
+                         0x3F800000, 0xBF800000], dtype=np.uint32).view(np.float32)
+    for _ in range(400):
+        R, V = int(rng.integers(1, 4)), int(rng.integers(1, 40))
+        x = rng.choice(specials, size=(R, V)).astype(np.float32)
+        with np.errstate(invalid="ignore"):
+            assert np.array_equal(oracle.argmax_rows(x), np.argmax(x, axis=1))
+        xb = (x.view(np.uint32) >> 16).astype(np.uint16)      # exact: low halves are zero
+        wide = (xb.astype(np.uint32) << 16).view(np.float32)
+        assert np.array_equal(oracle.argmax_rows(xb), np.argmax(wide, axis=1))
+    # every NaN pattern of bf16 ranks above +inf and below no other NaN
+    nans = np.array([0x7F81, 0x7FC0, 0x7FFF, 0xFF81, 0xFFC0, 0xFFFF], dtype=np.uint16)
+    for n in nans:
+        row = np.array([[0x7F80, n, 0x3F80, n ^ 0x8000]], dtype=np.uint16)
+        assert oracle.argmax_rows(row)[0] == 1
 
 
 def test_regret_is_one_fp32_subtraction():
