@@ -72,9 +72,10 @@ typedef struct {
  * draft_tokens    int32 [total_rows]: row o_i + p - 1 holds draft x_p of
  *                 request i (p = 1..K_i); the entry of each bonus row o_i + K_i
  *                 is ignored.
- * block_lens      int32 [num_requests]: K_i >= 0.
+ * block_lens      int32 [num_requests]: K_i >= 0 (a negative K_i is read as 0
+ *                 and reported in the device error word, see asd_device_error).
  * row_offsets     int64 [num_requests]: first row o_i of request i, or NULL for
- *                 the packed layout o_i = sum_{j<i} (K_j + 1).
+ *                 the packed layout o_i = sum_{j<i} (max(K_j, 0) + 1).
  * tau             float [num_requests]: the local gate g_i of Eq. 7.
  * exc_cap         int32 [num_requests]: the block cap M_i of Eq. 10
  *                 (INT32_MAX acts as no cap).
@@ -92,16 +93,21 @@ typedef struct {
  * stream          a hipStream_t, or NULL.
  *
  * Semantics (bit-exact with the CPU oracle):
- *  - argmax order: the numeric order with -0 == +0; a NaN with the sign bit
- *    clear ranks above +inf and one with it set below -inf, NaNs of one sign
- *    ordered by payload (IEEE 754 totalOrder).
+ *  - argmax order: the numeric order with -0 == +0; every NaN, of either sign
+ *    and any payload, ranks above +inf and equal to every other NaN, so a
+ *    row's first NaN is its argmax (numpy.argmax's convention).  A row whose
+ *    greatest logit is NaN has a NaN regret, and a NaN regret never passes
+ *    the gate.
  *  - gate r_i <= g_i * q_i is decided exactly (binary64); budget as
  *    fl32(s + C_t) <= B; cap as N_t <= M; C_t is a binary32 running sum in
  *    position order; s' = fl32(s + C_a).
  *  - B == 0 (either sign): exact greedy verification, ledger unchanged.
  *  - a draft id outside [0, V) is a mismatch that is never accepted.
- *  - a request with K_i < 0, o_i < 0 or o_i + K_i >= total_rows is not
- *    verified: a_i = 0, next token = -1, ledger untouched.
+ *  - K_i < 0 is read as K_i = 0: the request's one row is its bonus row,
+ *    a_i = 0 and the next token is that row's argmax.
+ *  - a request with o_i < 0 or o_i + K_i >= total_rows is not verified:
+ *    a_i = 0, next token = -1, ledger untouched.
+ *  Both cases also set a bit of the device error word (asd_device_error).
  *
  * Outputs must not alias the inputs.  Calls that share the library workspace
  * of one (device, stream) pair are ordered by the stream; calls on different
@@ -144,6 +150,60 @@ asd_status asd_verify_ws(const void *logits, asd_dtype dtype, int64_t vocab,
                          int32_t *out_accept_len, int32_t *out_next_token,
                          int32_t *out_argmax, float *out_regret, void *stream,
                          void *workspace, size_t workspace_bytes);
+
+/* Flags of asd_verify_ex. */
+enum {
+    ASD_GATE_RAW = 1   /* gate on the raw regret r_i <= g_i instead of Eq. 7's
+                          normalized r_i / q_i <= g_i (q_i read as 1) */
+};
+
+/*
+ * asd_verify_ex -- asd_verify with flags and an optional caller workspace.
+ *
+ * flags            0 (the paper's gate, Eqs. 7 and 11: identical to asd_verify)
+ *                  or ASD_GATE_RAW, a variant that gates every accepted
+ *                  mismatch on r_i <= g_i; budget, cap, dispatch and ledger are
+ *                  unchanged.  Unknown bits return ASD_EINVAL.
+ * workspace        NULL: the library workspace of (device, stream), as for
+ *                  asd_verify.  Otherwise as for asd_verify_ws (256-byte
+ *                  aligned, workspace_bytes >= asd_workspace_bytes(...)), and
+ *                  the call allocates nothing.
+ * The other arguments and all outputs are those of asd_verify.
+ */
+asd_status asd_verify_ex(const void *logits, asd_dtype dtype, int64_t vocab,
+                         int32_t num_requests, int64_t total_rows,
+                         const int32_t *draft_tokens, const int32_t *block_lens,
+                         const int64_t *row_offsets, const float *tau,
+                         const int32_t *exc_cap, asd_budget *budget_inout,
+                         int32_t *out_accept_len, int32_t *out_next_token,
+                         int32_t *out_argmax, float *out_regret, uint32_t flags,
+                         void *stream, void *workspace, size_t workspace_bytes);
+
+/* Bits of the device error word. */
+enum {
+    ASD_DEVERR_NEGATIVE_K = 1,   /* a request had K_i < 0 (read as 0) */
+    ASD_DEVERR_ROWS = 2,         /* a request's rows lay outside [0, total_rows)
+                                    (not verified, or not committed) */
+    ASD_DEVERR_COMMIT = 4        /* a verified request committed nothing: its
+                                    tokens did not fit below capacity, seq_len_i
+                                    was negative or a_i lay outside [0, K_i] */
+};
+
+/*
+ * asd_device_error -- read the sticky error word of the current device.
+ *
+ * The kernels OR ASD_DEVERR_* bits into one word per device when they meet
+ * data that has a defined but unusual reading (the calls still complete and
+ * return their documented outputs).  The word is shared by every call on the
+ * device, from any stream, and keeps its bits until cleared.
+ * out_word        host uint32: the word once all work enqueued on `stream` so
+ *                 far has completed.
+ * clear           nonzero: reset the word to 0 after reading it (in stream
+ *                 order; calls on other streams may set bits again at any time).
+ * Synchronizes `stream`, so it must not be called during stream capture
+ * (ASD_ECAPTURE).  ASD_EINVAL for a NULL out_word.
+ */
+asd_status asd_device_error(uint32_t *out_word, int32_t clear, void *stream);
 
 /*
  * Vocabulary-sharded (tensor-parallel) verification.  The verifier needs, per
@@ -244,9 +304,11 @@ asd_status asd_opportunity(const int32_t *draft_tokens, const int32_t *row_argma
  * seq_len         int64 [num_requests]: committed lengths, advanced in place.
  * out_committed   int32 [num_requests] or NULL: a_i + 1, or 0 for a request that
  *                 commits nothing.
- * A request commits nothing when its rows do not fit in [0, total_rows), its
- * next_token is negative (not verified), a_i lies outside [0, K_i], seq_len_i is
- * negative, or the a_i + 1 tokens do not fit below capacity.  Allocates nothing;
+ * A negative K_i is read as 0, as asd_verify reads it.  A request commits
+ * nothing when its rows do not fit in [0, total_rows), its next_token is
+ * negative (not verified), a_i lies outside [0, K_i], seq_len_i is negative, or
+ * the a_i + 1 tokens do not fit below capacity; each case but a negative
+ * next_token sets a bit of the device error word.  Allocates nothing;
  * asynchronous on `stream`, so it can follow asd_verify in one captured graph.
  */
 asd_status asd_commit(const int32_t *draft_tokens, const int32_t *block_lens,
@@ -264,7 +326,7 @@ asd_status asd_commit(const int32_t *draft_tokens, const int32_t *block_lens,
  * row_offsets == NULL, has no request limit).  tokens, capacity, seq_len and
  * out_committed are those of asd_commit, with the same rules: a request
  * commits nothing when it is not verified, its a_i + 1 tokens do not fit below
- * capacity, or seq_len_i is negative.
+ * capacity, or seq_len_i is negative (the last two set ASD_DEVERR_COMMIT).
  * workspace       NULL: the library workspace of (device, stream), allocated on
  *                 first use and never during stream capture, as for asd_verify.
  *                 Otherwise caller memory of workspace_bytes >=
@@ -312,7 +374,7 @@ asd_status asd_lmhead_verify(const void *hidden, const void *weight, int64_t d, 
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 
-/* Library version string, e.g. "asd-mi355x 0.1.0 gfx950" (static storage). */
+/* Library version string, e.g. "asd-mi355x 0.3.0 gfx950" (static storage). */
 const char *asd_version(void);
 
 /*

@@ -13,13 +13,18 @@ import torch
 
 from .build import LIBRARY
 
-__all__ = ["asd_verify", "asd_verify_ws", "asd_shard_argmax", "asd_verify_partials",
-           "asd_opportunity", "asd_commit", "asd_verify_commit", "asd_lmhead_verify",
-           "asd_workspace_bytes", "asd_status_string", "asd_version", "asd_release", "AsdError",
-           "ASD_F32", "ASD_BF16", "library_path"]
+__all__ = ["asd_verify", "asd_verify_ws", "asd_verify_ex", "asd_shard_argmax",
+           "asd_verify_partials", "asd_opportunity", "asd_commit", "asd_verify_commit",
+           "asd_lmhead_verify", "asd_device_error", "asd_workspace_bytes", "asd_status_string",
+           "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16", "ASD_GATE_RAW",
+           "ASD_DEVERR_NEGATIVE_K", "ASD_DEVERR_ROWS", "ASD_DEVERR_COMMIT", "library_path"]
 
 ASD_F32 = 0
 ASD_BF16 = 1
+ASD_GATE_RAW = 1            # asd_verify_ex flag: gate on r <= g instead of r / q <= g
+ASD_DEVERR_NEGATIVE_K = 1   # device error word bits (asd_device_error)
+ASD_DEVERR_ROWS = 2
+ASD_DEVERR_COMMIT = 4
 _DTYPES = {torch.float32: ASD_F32, torch.bfloat16: ASD_BF16}
 
 _lib = None
@@ -49,6 +54,10 @@ def _load():
     lib.asd_verify.restype = ctypes.c_int
     lib.asd_verify_ws.argtypes = common + [vp, sz]
     lib.asd_verify_ws.restype = ctypes.c_int
+    lib.asd_verify_ex.argtypes = common[:-1] + [ctypes.c_uint32, vp, vp, sz]
+    lib.asd_verify_ex.restype = ctypes.c_int
+    lib.asd_device_error.argtypes = [vp, i32, vp]
+    lib.asd_device_error.restype = ctypes.c_int
     lib.asd_shard_argmax.argtypes = [vp, ctypes.c_int, i64, i64, i64, i64, vp, vp, vp]
     lib.asd_shard_argmax.restype = ctypes.c_int
     lib.asd_verify_partials.argtypes = [vp, i32, i64, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp,
@@ -183,7 +192,7 @@ def asd_verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, *, row_of
 def asd_verify_ws(logits, draft_tokens, block_lens, tau, exc_cap, budget, workspace, *,
                   row_offsets=None, out_accept_len=None, out_next_token=None, out_argmax=None,
                   out_regret=None):
-    """``asd_verify`` with a caller-provided workspace (a zero-initialised uint8 tensor)."""
+    """``asd_verify`` with a caller-provided workspace (a uint8 tensor, any content)."""
     if workspace.dtype != torch.uint8 or not workspace.is_contiguous():
         raise ValueError("workspace must be a contiguous uint8 tensor")
     _check_logits(logits)
@@ -198,6 +207,44 @@ def asd_verify_ws(logits, draft_tokens, block_lens, tau, exc_cap, budget, worksp
     if st != 0:
         raise AsdError(st, "asd_verify_ws")
     return acc, nxt
+
+
+def asd_verify_ex(logits, draft_tokens, block_lens, tau, exc_cap, budget, *, flags=0,
+                  workspace=None, row_offsets=None, out_accept_len=None, out_next_token=None,
+                  out_argmax=None, out_regret=None):
+    """``asd_verify`` with flags (``ASD_GATE_RAW``) and an optional workspace
+    (``asd_verify_ex`` of ``include/asd.h``)."""
+    if workspace is not None and (workspace.dtype != torch.uint8 or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous uint8 tensor")
+    _check_logits(logits)
+    with torch.cuda.device(logits.device):
+        args, acc, nxt, keep = _marshal(logits.device, logits.shape[0], draft_tokens, block_lens,
+                                        tau, exc_cap, budget, row_offsets, out_accept_len,
+                                        out_next_token, out_argmax, out_regret)
+        ws = None if workspace is None else ctypes.c_void_p(workspace.data_ptr())
+        ws_bytes = 0 if workspace is None else workspace.numel()
+        st = _load().asd_verify_ex(ctypes.c_void_p(logits.data_ptr()), _DTYPES[logits.dtype],
+                                   logits.shape[1], *args[:-1], int(flags), args[-1], ws,
+                                   ws_bytes)
+    del keep
+    if st != 0:
+        raise AsdError(st, "asd_verify_ex")
+    return acc, nxt
+
+
+def asd_device_error(clear=False, device=None) -> int:
+    """The sticky error word of a device (``asd_device_error``): ``ASD_DEVERR_*``
+    bits, read once the current stream's work has completed; ``clear`` resets it."""
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None \
+        else torch.device(device)
+    word = ctypes.c_uint32(0)
+    with torch.cuda.device(dev):
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        st = _load().asd_device_error(ctypes.byref(word), 1 if clear else 0,
+                                      ctypes.c_void_p(stream))
+    if st != 0:
+        raise AsdError(st, "asd_device_error")
+    return int(word.value)
 
 
 def asd_shard_argmax(shard_logits, vocab_offset, vocab, draft_tokens, out_partials=None):

@@ -77,6 +77,7 @@ struct Workspace {
 std::mutex g_mutex;
 std::map<std::pair<int, hipStream_t>, Workspace> g_workspaces;
 std::map<int, int> g_cu_count;
+std::map<int, uint32_t*> g_error_words;   // device -> address of its error word
 
 asd_status cu_count(int device, int* out) {
     auto it = g_cu_count.find(device);
@@ -126,7 +127,8 @@ asd_status enqueue(const void* logits, asd_dtype dtype, int64_t vocab, int32_t n
                    asd_budget* budget, int32_t* out_accept_len, int32_t* out_next_token,
                    int32_t* out_argmax, float* out_regret, hipStream_t stream, const Plan& plan,
                    void* workspace, int32_t* commit_tokens = nullptr, int64_t commit_capacity = 0,
-                   int64_t* commit_seq_len = nullptr, int32_t* commit_done = nullptr) {
+                   int64_t* commit_seq_len = nullptr, int32_t* commit_done = nullptr,
+                   bool raw_gate = false) {
     CallArgs a;
     a.logits = logits;
     a.num_requests = num_requests;
@@ -144,6 +146,7 @@ asd_status enqueue(const void* logits, asd_dtype dtype, int64_t vocab, int32_t n
     a.commit_capacity = commit_capacity;
     a.commit_seq_len = commit_seq_len;
     a.commit_done = commit_done;
+    a.raw_gate = raw_gate;
     (void)dtype;
     (void)vocab;
     (void)total_rows;
@@ -192,6 +195,18 @@ asd_status library_workspace(hipStream_t s, size_t bytes, void** out) {
     }
     *out = w.ptr;
     return ASD_OK;
+}
+
+// The caller's workspace when given (size checked; its alignment is checked
+// with the other host arguments), else the library's.
+asd_status resolve_workspace(hipStream_t s, const Plan& plan, void* workspace,
+                             size_t workspace_bytes, void** out) {
+    if (workspace) {
+        if (workspace_bytes < plan.ws_bytes) return ASD_ENOMEM;
+        *out = workspace;
+        return ASD_OK;
+    }
+    return library_workspace(s, plan.ws_bytes, out);
 }
 
 }  // namespace
@@ -251,6 +266,59 @@ asd_status asd_verify_ws(const void* logits, asd_dtype dtype, int64_t vocab,
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
                    out_argmax, out_regret, (hipStream_t)stream, plan, workspace);
+}
+
+asd_status asd_verify_ex(const void* logits, asd_dtype dtype, int64_t vocab,
+                         int32_t num_requests, int64_t total_rows, const int32_t* draft_tokens,
+                         const int32_t* block_lens, const int64_t* row_offsets, const float* tau,
+                         const int32_t* exc_cap, asd_budget* budget_inout,
+                         int32_t* out_accept_len, int32_t* out_next_token, int32_t* out_argmax,
+                         float* out_regret, uint32_t flags, void* stream, void* workspace,
+                         size_t workspace_bytes) {
+    asd_status st = check_args(logits, dtype, vocab, num_requests, total_rows, draft_tokens,
+                               block_lens, tau, exc_cap, budget_inout, out_accept_len,
+                               out_next_token);
+    if (st != ASD_OK) return st;
+    if ((flags & ~(uint32_t)ASD_GATE_RAW) != 0) return ASD_EINVAL;
+    if (num_requests == 0) return ASD_OK;
+    if (workspace && ((uintptr_t)workspace & 255) != 0) return ASD_EINVAL;
+    Plan plan;
+    if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = nullptr;
+    if ((st = resolve_workspace(s, plan, workspace, workspace_bytes, &ws)) != ASD_OK) return st;
+    return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
+                   row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
+                   out_argmax, out_regret, s, plan, ws, nullptr, 0, nullptr, nullptr,
+                   (flags & ASD_GATE_RAW) != 0);
+}
+
+asd_status asd_device_error(uint32_t* out_word, int32_t clear, void* stream) {
+    if (!out_word) return ASD_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ASD_EHIP;
+    if (cap != hipStreamCaptureStatusNone) return ASD_ECAPTURE;
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return ASD_EHIP;
+    uint32_t* word = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_mutex);
+        auto it = g_error_words.find(device);
+        if (it == g_error_words.end()) {
+            if (error_word_address(&word) != hipSuccess || !word) return ASD_EHIP;
+            g_error_words[device] = word;
+        } else {
+            word = it->second;
+        }
+    }
+    uint32_t host = 0;
+    if (hipMemcpyAsync(&host, word, sizeof host, hipMemcpyDeviceToHost, s) != hipSuccess)
+        return ASD_EHIP;
+    if (clear && hipMemsetAsync(word, 0, sizeof host, s) != hipSuccess) return ASD_EHIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return ASD_EHIP;
+    *out_word = host;
+    return ASD_OK;
 }
 
 asd_status asd_shard_argmax(const void* shard_logits, asd_dtype dtype, int64_t shard_vocab,
@@ -379,12 +447,8 @@ asd_status asd_verify_commit(const void* logits, asd_dtype dtype, int64_t vocab,
     Plan plan;
     if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
     hipStream_t s = (hipStream_t)stream;
-    void* ws = workspace;
-    if (ws) {
-        if (workspace_bytes < plan.ws_bytes) return ASD_ENOMEM;
-    } else if ((st = library_workspace(s, plan.ws_bytes, &ws)) != ASD_OK) {
-        return st;
-    }
+    void* ws = nullptr;
+    if ((st = resolve_workspace(s, plan, workspace, workspace_bytes, &ws)) != ASD_OK) return st;
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
                    out_argmax, out_regret, s, plan, ws, tokens, capacity, seq_len, out_committed);
@@ -440,7 +504,7 @@ const char* asd_status_string(asd_status status) {
     }
 }
 
-const char* asd_version(void) { return "asd-mi355x 0.2.0 gfx950"; }
+const char* asd_version(void) { return "asd-mi355x 0.3.0 gfx950"; }
 
 asd_status asd_release(void) {
     std::lock_guard<std::mutex> lock(g_mutex);

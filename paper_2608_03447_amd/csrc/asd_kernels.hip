@@ -28,6 +28,15 @@
 #include "asd_plan.h"
 
 namespace asd {
+
+// Sticky error word of this device: the kernels OR in kErr* bits when they meet
+// data that the verifier reads in a defined but unusual way.
+__device__ uint32_t asd_error_word;
+
+hipError_t error_word_address(uint32_t** ptr) {
+    return hipGetSymbolAddress((void**)ptr, HIP_SYMBOL(asd_error_word));
+}
+
 namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -42,11 +51,55 @@ constexpr int kWaves = kRowThreads / 64;
 // ------------------------------------------------------------ integer keys
 //
 // key(x) is an integer that orders logits the way the argmax must: numeric
-// order with -0 == +0, positive NaNs above +inf and negative NaNs below -inf
-// (IEEE totalOrder for NaNs).  For a sign-magnitude pattern: key = magnitude
-// when the sign is clear, key = -magnitude when it is set.
+// order with -0 == +0, and every NaN, of either sign and any payload, above
+// +inf and equal to every other NaN (so a row's first NaN is its argmax).  For
+// a number's sign-magnitude pattern: key = magnitude when the sign is clear,
+// key = -magnitude when it is set; every NaN has the key kNan, one above +inf's.
 
-// Two bf16 keys at once, one per 16-bit half (packed 16-bit integer ops).
+// Smallest key of each dtype (below every key a real logit can have), the key
+// of +inf, the key of every NaN, and the greatest pattern that is not a NaN
+// with the sign bit set (-inf's).
+template <int EB> struct KeyTraits;
+template <> struct KeyTraits<2> {
+    static constexpr int32_t kNone = -0x8000;         // bf16 keys lie in [-0x7f80, 0x7f81]
+    static constexpr uint32_t kNonePacked = 0x80008000u;
+    static constexpr int32_t kInf = 0x7f80;
+    static constexpr int32_t kNan = 0x7f81;
+    static constexpr uint32_t kNegInfPattern = 0xff80u;
+};
+template <> struct KeyTraits<4> {
+    static constexpr int32_t kNone = (int32_t)0x80000000;   // f32 keys >= -0x7f800000
+    static constexpr int32_t kInf = 0x7f800000;
+    static constexpr int32_t kNan = 0x7f800001;
+    static constexpr uint32_t kNegInfPattern = 0xff800000u;
+};
+
+// The key of every binary32 pattern (used where one pass must rank anything).
+__device__ __forceinline__ int32_t f32_key(uint32_t u) {
+    const uint32_t mag = u & 0x7fffffffu;
+    const int32_t key = (int32_t)u < 0 ? -(int32_t)mag : (int32_t)mag;
+    return mag > 0x7f800000u ? KeyTraits<4>::kNan : key;
+}
+
+// Three ways to rank the logits of a row tile, cheapest first.
+//  kKeysRaw:   the raw bit patterns read as signed integers.  For every pattern
+//              with the sign bit clear that is neither +0 nor a NaN this equals
+//              the key, and every pattern with the sign bit set reads as
+//              negative.  So when the tile holds a pattern in [1, +inf] and no
+//              NaN, the raw maximum is the exact maximum, found with one
+//              integer max per element.  The raw pass also keeps the greatest
+//              pattern read as unsigned, which exceeds -inf's exactly when a
+//              NaN with the sign bit set is present (a NaN with it clear shows
+//              in the raw maximum).
+//  kKeysExact: sign-magnitude keys, exact for every number (tiles whose raw
+//              maximum is below 1 and that hold no NaN).
+//  kKeysNan:   min(magnitude, kNan): every NaN gets kNan and every number a
+//              smaller key, so in a tile known to hold a NaN the greatest key
+//              is kNan and its first element is the tile's first NaN.
+constexpr int kKeysRaw = 0, kKeysExact = 1, kKeysNan = 2;
+constexpr int32_t kRawExactFrom = 1;
+
+// Two bf16 sign-magnitude keys at once, one per 16-bit half.
 __device__ __forceinline__ uint32_t bf16x2_keys(uint32_t w) {
     const u16x2 v = __builtin_bit_cast(u16x2, w);
     const u16x2 neg = (u16x2)(unsigned short)0x8000 - v;       // -magnitude, mod 2^16
@@ -54,60 +107,52 @@ __device__ __forceinline__ uint32_t bf16x2_keys(uint32_t w) {
     return __builtin_bit_cast(uint32_t, (neg & sign) | (v & ~sign));
 }
 
-__device__ __forceinline__ int32_t f32_key(uint32_t u) {
-    const uint32_t sign = (uint32_t)((int32_t)u >> 31);
-    return (int32_t)(((0x80000000u - u) & sign) | (u & ~sign));
-}
-
-__device__ __forceinline__ int32_t bf16_key(uint32_t h16) {
-    return (int32_t)(int16_t)(bf16x2_keys(h16) & 0xffffu);
-}
-
 __device__ __forceinline__ uint32_t pkmax16(uint32_t a, uint32_t b) {
     return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, a),
                                                                   __builtin_bit_cast(s16x2, b)));
 }
 
-// Smallest key of each dtype: below every key a real logit can have.
-template <int EB> struct KeyTraits;
-template <> struct KeyTraits<2> {
-    static constexpr int32_t kNone = -0x8000;         // bf16 keys lie in [-0x7fff, 0x7fff]
-    static constexpr uint32_t kNonePacked = 0x80008000u;
-};
-template <> struct KeyTraits<4> {
-    static constexpr int32_t kNone = (int32_t)0x80000000;   // f32 keys >= -0x7fffffff
-};
-
-// Two ways to rank the logits of a tile.
-//  kRaw = false: the exact keys above.
-//  kRaw = true:  the raw bit patterns read as signed integers.  For every
-//                pattern with the sign bit clear (+0 aside) this equals the
-//                exact key, and every pattern with the sign bit set reads as
-//                negative.  So when the tile holds any pattern >= 1 (a positive
-//                value or positive NaN), the raw maximum is the exact maximum,
-//                found with one integer max per element instead of four ops.
-//                Tiles without one are ranked again with exact keys.
-constexpr int32_t kRawExactFrom = 1;
-
-template <int EB, bool kRaw>
-__device__ __forceinline__ uint32_t dword_keys(uint32_t w) {
-    if constexpr (kRaw) return w;
-    else if constexpr (EB == 2) return bf16x2_keys(w);
-    else return (uint32_t)f32_key(w);
+__device__ __forceinline__ uint32_t pkmaxu16(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, a),
+                                                                  __builtin_bit_cast(u16x2, b)));
 }
 
-// Max key over the 16-byte vectors of one group; vectors u >= nvalid are ignored.
-template <int EB, bool kRaw, bool kMasked>
-__device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], int nvalid) {
+__device__ __forceinline__ uint32_t pkminu16(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(__builtin_bit_cast(u16x2, a),
+                                                                  __builtin_bit_cast(u16x2, b)));
+}
+
+template <int EB, int kMode>
+__device__ __forceinline__ uint32_t dword_keys(uint32_t w) {
+    if constexpr (kMode == kKeysRaw) {
+        return w;
+    } else if constexpr (kMode == kKeysExact) {
+        if constexpr (EB == 2) return bf16x2_keys(w);
+        else return (int32_t)w < 0 ? 0x80000000u - w : w;
+    } else {
+        if constexpr (EB == 2) return pkminu16(w & 0x7fff7fffu, 0x7f817f81u);
+        else return min(w & 0x7fffffffu, (uint32_t)KeyTraits<4>::kNan);
+    }
+}
+
+// Max key over the 16-byte vectors of one group; vectors u >= nvalid are
+// ignored.  In the raw pass `umax` also takes the greatest pattern read as
+// unsigned (per 16-bit half for bf16); masked vectors hold zero and leave it.
+template <int EB, int kMode, bool kMasked>
+__device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], int nvalid,
+                                                 uint32_t& umax) {
     if constexpr (EB == 2) {
         uint32_t acc = KeyTraits<2>::kNonePacked;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const uint32_t k0 = dword_keys<2, kRaw>(raw[u].x), k1 = dword_keys<2, kRaw>(raw[u].y);
-            const uint32_t k2 = dword_keys<2, kRaw>(raw[u].z), k3 = dword_keys<2, kRaw>(raw[u].w);
+            const uint32_t k0 = dword_keys<2, kMode>(raw[u].x), k1 = dword_keys<2, kMode>(raw[u].y);
+            const uint32_t k2 = dword_keys<2, kMode>(raw[u].z), k3 = dword_keys<2, kMode>(raw[u].w);
             uint32_t m = pkmax16(pkmax16(k0, k1), pkmax16(k2, k3));
             if (kMasked && u >= nvalid) m = KeyTraits<2>::kNonePacked;
             acc = pkmax16(acc, m);
+            if constexpr (kMode == kKeysRaw)
+                umax = pkmaxu16(umax, pkmaxu16(pkmaxu16(raw[u].x, raw[u].y),
+                                               pkmaxu16(raw[u].z, raw[u].w)));
         }
         const int32_t lo = (int32_t)(int16_t)(acc & 0xffffu);
         const int32_t hi = (int32_t)acc >> 16;
@@ -116,47 +161,49 @@ __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], in
         int32_t acc = KeyTraits<4>::kNone;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            int32_t m = max(max((int32_t)dword_keys<4, kRaw>(raw[u].x),
-                                (int32_t)dword_keys<4, kRaw>(raw[u].y)),
-                            max((int32_t)dword_keys<4, kRaw>(raw[u].z),
-                                (int32_t)dword_keys<4, kRaw>(raw[u].w)));
+            int32_t m = max(max((int32_t)dword_keys<4, kMode>(raw[u].x),
+                                (int32_t)dword_keys<4, kMode>(raw[u].y)),
+                            max((int32_t)dword_keys<4, kMode>(raw[u].z),
+                                (int32_t)dword_keys<4, kMode>(raw[u].w)));
             if (kMasked && u >= nvalid) m = KeyTraits<4>::kNone;
             acc = max(acc, m);
+            if constexpr (kMode == kKeysRaw)
+                umax = max(umax, max(max(raw[u].x, raw[u].y), max(raw[u].z, raw[u].w)));
         }
         return acc;
     }
 }
 
 // Key of a bf16 bit pattern (low 16 bits of h16) or f32 bit pattern.
-template <int EB, bool kRaw>
+template <int EB, int kMode>
 __device__ __forceinline__ int32_t key_of(uint32_t pattern) {
-    if constexpr (EB == 2) return kRaw ? (int32_t)(int16_t)pattern : bf16_key(pattern);
-    else return kRaw ? (int32_t)pattern : f32_key(pattern);
+    if constexpr (EB == 2) return (int32_t)(int16_t)(dword_keys<2, kMode>(pattern) & 0xffffu);
+    else return (int32_t)dword_keys<4, kMode>(pattern);
 }
 
 // Element e of a 16-byte vector as (key, binary32 bits).
-template <int EB, bool kRaw>
+template <int EB, int kMode>
 __device__ __forceinline__ void element_of(const u32x4& v, int e, int32_t& key, uint32_t& bits) {
     if constexpr (EB == 2) {
         const uint32_t w = v[e >> 1];
         const uint32_t h = (e & 1) ? (w >> 16) : (w & 0xffffu);
-        key = key_of<2, kRaw>(h);
+        key = key_of<2, kMode>(h);
         bits = h << 16;
     } else {
         bits = v[e];
-        key = key_of<4, kRaw>(bits);
+        key = key_of<4, kMode>(bits);
     }
 }
 
-template <int EB, bool kRaw>
+template <int EB, int kMode>
 __device__ __forceinline__ void load_scalar(const unsigned char* p, int32_t& key, uint32_t& bits) {
     if constexpr (EB == 2) {
         const uint32_t h = *(const unsigned short*)p;
-        key = key_of<2, kRaw>(h);
+        key = key_of<2, kMode>(h);
         bits = h << 16;
     } else {
         bits = *(const uint32_t*)p;
-        key = key_of<4, kRaw>(bits);
+        key = key_of<4, kMode>(bits);
     }
 }
 
@@ -262,12 +309,16 @@ __device__ void write_packed_offsets(int32_t num_requests, const int32_t* __rest
 
 // One lane's best (key, column) and bits over its share of a tile: the
 // tile's 16-byte vectors [split * chunk_vecs, ...) of the row's aligned middle,
-// plus the row's unaligned head (split 0) and tail (last split) elements.
-template <int EB, bool kRaw>
+// plus the row's unaligned head (split 0) and tail (last split) elements.  In
+// the raw pass `nan_seen` tells whether the lane's share holds a NaN that the
+// raw maximum does not show (one with the sign bit set, or any NaN among the
+// head and tail elements); the other passes leave it alone.
+template <int EB, int kMode>
 __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const RowGeom& geom,
                                           int64_t vocab, int64_t col_offset, int split,
                                           int splits, int64_t chunk_vecs, int tid,
-                                          unsigned long long& packed, uint32_t& bits) {
+                                          unsigned long long& packed, uint32_t& bits,
+                                          bool& nan_seen) {
     constexpr int kEpv = 16 / EB;
     // stream this tile's 16-byte vectors
     const u32x4* vec = (const u32x4*)(row_ptr + geom.head * EB);
@@ -276,9 +327,10 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
     const int64_t nv = v1 > v0 ? v1 - v0 : 0;
     const int64_t nfull = nv / kGroupVecs;
 
-    int32_t best_key = kRaw ? KeyTraits<4>::kNone : KeyTraits<EB>::kNone;
+    int32_t best_key = kMode == kKeysRaw ? KeyTraits<4>::kNone : KeyTraits<EB>::kNone;
     int64_t best_group = -1;
     int best_nvalid = 0;
+    uint32_t umax = 0;
     u32x4 saved[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) saved[u] = (u32x4)(0u);
@@ -288,7 +340,9 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
         u32x4 raw[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) raw[u] = __builtin_nontemporal_load(p + u * kRowThreads);
-        const int32_t gk = group_max_key<EB, kRaw, false>(raw, kUnroll);
+        // All of the group's loads issue before any of them is waited for.
+        __builtin_amdgcn_sched_barrier(0);
+        const int32_t gk = group_max_key<EB, kMode, false>(raw, kUnroll, umax);
         const bool better = gk > best_key;
         best_key = better ? gk : best_key;
         best_group = better ? g : best_group;
@@ -310,7 +364,7 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
                 ++nvalid;
             }
         }
-        const int32_t gk = group_max_key<EB, kRaw, true>(raw, nvalid);
+        const int32_t gk = group_max_key<EB, kMode, true>(raw, nvalid, umax);
         if (nvalid > 0 && gk > best_key) {
             best_key = gk;
             best_group = g;
@@ -331,7 +385,7 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
             for (int e = 0; e < kEpv; ++e) {
                 int32_t k;
                 uint32_t b;
-                element_of<EB, kRaw>(saved[u], e, k, b);
+                element_of<EB, kMode>(saved[u], e, k, b);
                 if (!found && u < best_nvalid && k == best_key) {
                     found = true;
                     const int64_t vi = v0 + best_group * kGroupVecs + u * kRowThreads + tid;
@@ -342,19 +396,28 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
         }
     }
 
+    if constexpr (kMode == kKeysRaw) {
+        if constexpr (EB == 2)
+            nan_seen = max(umax & 0xffffu, umax >> 16) > KeyTraits<2>::kNegInfPattern;
+        else
+            nan_seen = umax > KeyTraits<4>::kNegInfPattern;
+    }
+
     // unaligned head and tail elements (at most 16 / EB - 1 of each)
     if (split == 0 && tid < geom.head) {
         int32_t k;
         uint32_t b;
-        load_scalar<EB, kRaw>(row_ptr + (int64_t)tid * EB, k, b);
+        load_scalar<EB, kMode>(row_ptr + (int64_t)tid * EB, k, b);
         take_better(packed, bits, pack_kc(k, col_offset + tid), b);
+        if constexpr (kMode == kKeysRaw) nan_seen = nan_seen || (b & 0x7fffffffu) > 0x7f800000u;
     }
     if (split == splits - 1 && tid < vocab - geom.tail) {
         const int64_t c = geom.tail + tid;
         int32_t k;
         uint32_t b;
-        load_scalar<EB, kRaw>(row_ptr + c * EB, k, b);
+        load_scalar<EB, kMode>(row_ptr + c * EB, k, b);
         take_better(packed, bits, pack_kc(k, col_offset + c), b);
+        if constexpr (kMode == kKeysRaw) nan_seen = nan_seen || (b & 0x7fffffffu) > 0x7f800000u;
     }
 
 }
@@ -368,7 +431,7 @@ template <int EB>
 // parallel shard); columns are reported globally.  With `partials` set every
 // tile writes a partial (split rows, or one shard of each row); otherwise each
 // row is one tile and writes its record.
-__global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(8))) void asd_row_kernel(
     const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
     int64_t chunk_vecs, const int32_t* __restrict__ draft_tokens,
     TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
@@ -394,22 +457,37 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_kernel(
     uint32_t draft_bits = 0;
     if (owns_x && tid == 0) {
         int32_t k_unused;
-        load_scalar<EB, true>(row_ptr + x_local * EB, k_unused, draft_bits);
+        load_scalar<EB, kKeysRaw>(row_ptr + x_local * EB, k_unused, draft_bits);
     }
 
-    // ---- rank the tile by raw patterns; if it holds no positive pattern the
-    // raw order is not the exact one, so rank it again with exact keys.
+    // ---- rank the tile by raw patterns.  If it holds a NaN, rank it again to
+    // find its first NaN; else if its raw maximum is below 1 (no positive
+    // number), rank it again with sign-magnitude keys.
     unsigned long long packed;
     uint32_t bits;
-    tile_best<EB, true>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid, packed,
-                        bits);
-    block_reduce(packed, bits);
-    __shared__ int s_exact;
-    if (tid == 0) s_exact = packed_key(packed) < kRawExactFrom;
+    bool nan_seen = false;
+    tile_best<EB, kKeysRaw>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
+                            packed, bits, nan_seen);
+    __shared__ int s_nan[kWaves];
+    const bool wave_nan = __ballot(nan_seen) != 0ull;
+    if ((tid & 63) == 0) s_nan[tid >> 6] = wave_nan;
+    block_reduce(packed, bits);          // its barrier also publishes s_nan
+    __shared__ int s_mode;
+    if (tid == 0) {
+        const int32_t k = packed_key(packed);
+        int any_nan = k > KeyTraits<EB>::kInf;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) any_nan |= s_nan[w];
+        s_mode = any_nan ? kKeysNan : (k < kRawExactFrom ? kKeysExact : kKeysRaw);
+    }
     __syncthreads();
-    if (s_exact) {
-        tile_best<EB, false>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
-                             packed, bits);
+    if (s_mode == kKeysExact) {
+        tile_best<EB, kKeysExact>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs,
+                                  tid, packed, bits, nan_seen);
+        block_reduce(packed, bits);
+    } else if (s_mode == kKeysNan) {
+        tile_best<EB, kKeysNan>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
+                                packed, bits, nan_seen);
         block_reduce(packed, bits);
     }
     if (tid != 0) return;
@@ -463,6 +541,7 @@ struct ScanArgs {
     int64_t commit_capacity;
     int64_t* commit_seq_len;
     int32_t* commit_done;
+    int raw_gate;                         // gate on r <= g (q read as 1)
     int32_t* out_accept_len;
     int32_t* out_next_token;
     float* out_regret;
@@ -535,7 +614,8 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
 
     const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
     if (i >= A.num_requests) return;
-    const int32_t K = A.block_lens[i];
+    const int32_t K_given = A.block_lens[i];
+    const int32_t K = K_given > 0 ? K_given : 0;      // a negative K is read as 0
     int64_t o;
     if (A.offsets) {
         o = A.offsets[i];
@@ -553,11 +633,13 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         o = part;
     }
     const int64_t L = A.commit_tokens ? A.commit_seq_len[i] : 0;   // loaded early
-    if (!(K >= 0 && o >= 0 && o + (int64_t)K < A.total_rows)) {
+    if (K_given < 0 && lane == 0) atomicOr(&asd_error_word, kErrNegativeK);
+    if (!(o >= 0 && o + (int64_t)K < A.total_rows)) {
         if (lane == 0) {
             A.out_accept_len[i] = 0;
             A.out_next_token[i] = -1;
             if (A.commit_tokens && A.commit_done) A.commit_done[i] = 0;
+            atomicOr(&asd_error_word, kErrRows);
         }
         return;
     }
@@ -601,8 +683,10 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         if (done) continue;
 
         // Mismatches among this chunk's draft positions, and those that pass
-        // the local gate r <= g q (q = K - p, i.e. K - i + 1 for i = p + 1).
-        const bool gate = (double)r <= (double)g * (double)(int32_t)(K - (int32_t)p);
+        // the local gate r <= g q (q = K - p, i.e. K - i + 1 for i = p + 1;
+        // q = 1 for the raw-gate variant).
+        const int32_t q = A.raw_gate ? 1 : K - (int32_t)p;
+        const bool gate = (double)r <= (double)g * (double)q;
         const unsigned long long mism_mask = __ballot(is_draft && mism);
         const unsigned long long ok_mask = __ballot(is_draft && mism && !bad && gate);
         int stop = -1;
@@ -649,6 +733,7 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         if (lane == 0) {
             if (ok) A.commit_seq_len[i] = L + (int64_t)a + 1;
             if (A.commit_done) A.commit_done[i] = ok ? a + 1 : 0;
+            if (!ok) atomicOr(&asd_error_word, kErrCommit);
         }
     }
 }
@@ -681,6 +766,7 @@ ScanArgs scan_args(const CallArgs& a, int64_t rows, int64_t vocab, int elem_byte
     A.commit_capacity = a.commit_capacity;
     A.commit_seq_len = a.commit_seq_len;
     A.commit_done = a.commit_done;
+    A.raw_gate = a.raw_gate ? 1 : 0;
     return A;
 }
 
@@ -809,7 +895,8 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
     if (i >= num_requests) return;
-    const int32_t K = block_lens[i];
+    const int32_t K_given = block_lens[i];
+    const int32_t K = K_given > 0 ? K_given : 0;      // a negative K is read as 0
     int64_t o;
     if (row_offsets) {
         o = row_offsets[i];
@@ -826,8 +913,9 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
     const int32_t a = accept_len[i];
     const int32_t next = next_token[i];
     const int64_t L = seq_len[i];
-    const bool ok = K >= 0 && o >= 0 && o + (int64_t)K < total_rows && next >= 0 && L >= 0 &&
-                    a >= 0 && a <= K && L + (int64_t)a + 1 <= capacity;
+    const bool rows_ok = o >= 0 && o + (int64_t)K < total_rows;
+    const bool ok = rows_ok && next >= 0 && L >= 0 && a >= 0 && a <= K &&
+                    L + (int64_t)a + 1 <= capacity;
     if (ok) {
         int32_t* dst = tokens + i * capacity + L;
         for (int64_t j = lane; j <= a; j += 64) dst[j] = j < a ? draft_tokens[o + j] : next;
@@ -835,6 +923,9 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
     if (lane == 0) {
         if (ok) seq_len[i] = L + (int64_t)a + 1;
         if (committed) committed[i] = ok ? a + 1 : 0;
+        const uint32_t err = (K_given < 0 ? kErrNegativeK : 0u) | (rows_ok ? 0u : kErrRows) |
+                             (rows_ok && next >= 0 && !ok ? kErrCommit : 0u);
+        if (err) atomicOr(&asd_error_word, err);
     }
 }
 
@@ -1024,7 +1115,8 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
     // E1 those of wm = 1, each [32 rows][256 columns] of logit bits, with the
     // 16-B chunk c of row lr at chunk c ^ ((c >> 4) & 3) ^ 4 (lr & 3) ^
     // 8 ((lr >> 2) & 1): conflict-free for the stores and for the row scans.
-    // Columns past N are stored as 0xffffffff, the smallest key.  Then four
+    // Columns past N are stored as -inf, whose key no value ranks below; a real
+    // column that ties with one wins by its lower index.  Then four
     // threads scan each of the 64 rows, 64 columns each in increasing order.
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no copy outlives the main loop
     uint32_t* const E0 = (uint32_t*)A0;
@@ -1054,7 +1146,7 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
                 // cast of the vector element itself read element 0 for every v.
                 const float val = acc[i][j][v];
                 Ew[(wbase[j] ^ ((v & 3) << 4)) + 256 * (8 * (v >> 2) + (v & 3))] =
-                    __float_as_uint(val) | wmask[j];
+                    (__float_as_uint(val) & ~wmask[j]) | (0xff800000u & wmask[j]);
             }
         __syncthreads();
         const int r = (rr >> 5) * 128 + i * 32 + lrr;      // tile row

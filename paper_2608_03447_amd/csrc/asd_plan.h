@@ -33,6 +33,15 @@ struct alignas(8) RowRecord {
     float regret;
 };
 
+// Bits of the sticky per-device error word (the values of ASD_DEVERR_*).
+constexpr uint32_t kErrNegativeK = 1u;   // a request with K < 0, read as K = 0
+constexpr uint32_t kErrRows = 2u;        // a request whose rows lie outside the batch
+constexpr uint32_t kErrCommit = 4u;      // a verified request whose tokens were not committed
+
+// Address of this device's error word (device memory, 4 bytes), valid on the
+// device current at the call.
+hipError_t error_word_address(uint32_t** ptr);
+
 constexpr uint32_t kMismatchBit = 0x80000000u;
 constexpr uint32_t kBadDraftBit = 0x40000000u;
 constexpr uint32_t kArgmaxMask = 0x3fffffffu;
@@ -66,6 +75,7 @@ struct CallArgs {
     int32_t* out_next_token = nullptr;
     int32_t* out_argmax = nullptr;
     float* out_regret = nullptr;
+    bool raw_gate = false;             // gate on r <= g instead of r / q <= g
     // Commit in the same pass (asd_verify_commit); tokens == nullptr: none.
     int32_t* commit_tokens = nullptr;  // [num_requests][commit_capacity]
     int64_t commit_capacity = 0;

@@ -64,6 +64,16 @@ int main() {
     expect(asd_verify_ws(L, ASD_BF16, 100, 1, 2, D, K, nullptr, T, M, B, A, X, nullptr, nullptr,
                          nullptr, nullptr, 1 << 20), ASD_EINVAL, "verify_ws null workspace");
 
+    // flags and the device error word
+    expect(asd_verify_ex(L, ASD_BF16, 100, 1, 2, D, K, nullptr, T, M, B, A, X, nullptr, nullptr,
+                         2u, nullptr, nullptr, 0), ASD_EINVAL, "verify_ex unknown flag");
+    expect(asd_verify_ex(L, ASD_BF16, 100, 1, 2, D, K, nullptr, T, M, B, A, X, nullptr, nullptr,
+                         ASD_GATE_RAW, nullptr, fake<void>(0x90010), 1 << 20), ASD_EINVAL,
+           "verify_ex misaligned workspace");
+    expect(asd_verify_ex(L, ASD_BF16, 100, 0, 0, D, K, nullptr, T, M, B, A, X, nullptr, nullptr,
+                         ASD_GATE_RAW, nullptr, nullptr, 0), ASD_OK, "verify_ex empty");
+    expect(asd_device_error(nullptr, 1, nullptr), ASD_EINVAL, "device_error null output");
+
     // sharded form
     expect(asd_shard_argmax(L, ASD_BF16, 0, 0, 100, 2, D, fake<asd_row_partial>(0xa0000),
                             nullptr), ASD_EINVAL, "shard width 0");
@@ -115,6 +125,19 @@ int main() {
         }
         if (s != ASD_EHIP && s != ASD_ENOMEM) {
             std::fprintf(stderr, "verify without a device returned %s\n", asd_status_string(s));
+            ++failures;
+        }
+        const asd_status x = asd_verify_ex(L, ASD_BF16, 100, 1, 2, D, K, nullptr, T, M, B, A, X,
+                                           nullptr, nullptr, ASD_GATE_RAW, nullptr, nullptr, 0);
+        if (x != ASD_EHIP && x != ASD_ENOMEM) {
+            std::fprintf(stderr, "verify_ex without a device returned %s\n", asd_status_string(x));
+            ++failures;
+        }
+        uint32_t word = 0;
+        const asd_status e = asd_device_error(&word, 1, nullptr);
+        if (e != ASD_EHIP) {
+            std::fprintf(stderr, "device_error without a device returned %s\n",
+                         asd_status_string(e));
             ++failures;
         }
         const asd_status t = asd_lmhead_verify(L, L, 256, 100, 1, 2, D, K, nullptr, T, M, B, A,

@@ -15,8 +15,9 @@ def device_logits(logits, dev):
 
 
 def gpu_verify(logits, draft, lens, tau, cap, budget, row_offsets=None, dev="cuda:0",
-               workspace=None, stream=None):
-    """One asd_verify call; returns numpy outputs (budget = updated ledger)."""
+               workspace=None, stream=None, flags=None):
+    """One asd_verify call (asd_verify_ex when ``flags`` is given); returns
+    numpy outputs (budget = updated ledger)."""
     dev = torch.device(dev)
     n = len(lens)
     rows = logits.shape[0]
@@ -32,7 +33,10 @@ def gpu_verify(logits, draft, lens, tau, cap, budget, row_offsets=None, dev="cud
         np.ascontiguousarray(row_offsets, dtype=np.int64)).to(dev)
     amax = torch.full((rows,), -7, dtype=torch.int32, device=dev)
     regret = torch.full((rows,), float("nan"), dtype=torch.float32, device=dev)
-    if workspace is None:
+    if flags is not None:
+        acc, nxt = asd.asd_verify_ex(tl, td, tk, tt, tc, tb, flags=flags, workspace=workspace,
+                                     row_offsets=to, out_argmax=amax, out_regret=regret)
+    elif workspace is None:
         acc, nxt = asd.asd_verify(tl, td, tk, tt, tc, tb, row_offsets=to, out_argmax=amax,
                                   out_regret=regret)
     else:
@@ -44,8 +48,8 @@ def gpu_verify(logits, draft, lens, tau, cap, budget, row_offsets=None, dev="cud
             "budget": tb.cpu().numpy()}
 
 
-def oracle_verify(logits, draft, lens, tau, cap, budget, row_offsets=None):
-    return oracle.verify(logits, draft, lens, tau, cap, budget, row_offsets)
+def oracle_verify(logits, draft, lens, tau, cap, budget, row_offsets=None, raw_gate=False):
+    return oracle.verify(logits, draft, lens, tau, cap, budget, row_offsets, raw_gate=raw_gate)
 
 
 def mismatches(gpu, ref):

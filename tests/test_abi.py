@@ -275,3 +275,36 @@ def test_header_compiles_cleanly_as_c_and_cpp(tmp_path, lang):
     r = subprocess.run([cc, std, "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", inc, "-c",
                         str(src), "-o", str(tmp_path / "use.o")], capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def _call_ex(flags, ws=None, ws_bytes=0, **kw):
+    lib = asd._load()
+    a = dict(logits=0x1000, dtype=1, vocab=100, nreq=1, rows=2, draft=0x2000, lens=0x3000,
+             offs=None, tau=0x4000, cap=0x5000, budget=0x6000, acc=0x7000, nxt=0x8000,
+             amax=None, regret=None, stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_verify_ex(vp(a["logits"]), a["dtype"], a["vocab"], a["nreq"], a["rows"],
+                             vp(a["draft"]), vp(a["lens"]), vp(a["offs"]), vp(a["tau"]),
+                             vp(a["cap"]), vp(a["budget"]), vp(a["acc"]), vp(a["nxt"]),
+                             vp(a["amax"]), vp(a["regret"]), flags, vp(a["stream"]), vp(ws),
+                             ws_bytes)
+
+
+@pytest.mark.parametrize("flags", [2, 4, 0x80000000, 0xFFFFFFFF, 3])
+def test_verify_ex_rejects_unknown_flags(flags):
+    assert _call_ex(flags) == 1
+
+
+def test_verify_ex_checks_arguments_like_verify():
+    assert _call_ex(0, logits=None) == 1
+    assert _call_ex(1, dtype=5) == 2
+    assert _call_ex(1, nreq=0, rows=0, logits=None, draft=None) == 0     # empty: no-op
+    assert _call_ex(0, ws=0x10010, ws_bytes=1 << 20) == 1                # misaligned workspace
+
+
+def test_device_error_needs_an_output():
+    lib = asd._load()
+    assert lib.asd_device_error(None, 0, None) == 1
+    assert asd.ASD_GATE_RAW == 1
+    assert (asd.ASD_DEVERR_NEGATIVE_K, asd.ASD_DEVERR_ROWS, asd.ASD_DEVERR_COMMIT) == (1, 2, 4)

@@ -108,8 +108,9 @@ def test_verify_commit_matches_oracle_and_the_two_calls(cfg, library_ws):
 
 
 def test_verify_commit_with_offsets_and_unverified_requests():
-    """Explicit offsets with a gap, a request whose rows do not fit and one with
-    K < 0: those two commit nothing and keep their lengths."""
+    """Explicit offsets with a gap, requests whose rows do not fit (they commit
+    nothing and keep their lengths) and one with K < 0, read as K = 0 (it commits
+    its one emitted token)."""
     rng = np.random.default_rng(78)
     vocab, rows = 3000, 120
     z = rng.normal(0, 2, size=(rows, vocab)).astype(np.float32)
@@ -138,7 +139,7 @@ def test_verify_commit_with_offsets_and_unverified_requests():
     assert np.array_equal(tok.cpu().numpy(), r_tok)
     assert np.array_equal(sl.cpu().numpy(), r_sl)
     assert np.array_equal(done.cpu().numpy(), r_done)
-    assert list(r_done[[3, 5, 7]]) == [0, 0, 0]
+    assert list(r_done[[3, 5, 7]]) == [1, 0, 0]
 
 
 @pytest.mark.parametrize("fused", [False, True])

@@ -205,7 +205,8 @@ def test_explicit_row_offsets_with_gaps_and_invalid_requests():
     offs = np.array([0, 10, 12, 20, 30, 117, 100, -4], dtype=np.int64)
     budget = np.tile(np.array([[3.0, 0.5]], np.float32), (8, 1))
     g = check(logits, draft, lens, 2.0, 1, budget, row_offsets=offs, label="offsets")
-    assert list(g["next_token"][[3, 5, 7]]) == [-1, -1, -1]
+    assert list(g["next_token"][[5, 7]]) == [-1, -1]          # rows outside the batch
+    assert g["next_token"][3] == y[20] and g["accept_len"][3] == 0   # K = -1 read as 0
 
 
 def test_zero_length_blocks_emit_the_bonus_token():
