@@ -154,6 +154,61 @@ def copy_calibration(torch, nbytes=1 << 30, reps=10):
                       "reps": reps}), flush=True)
 
 
+def host_info():
+    """Host CPU model and logical CPU count, as the machine reports them."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count()}
+
+
+def threaded_oracle(w, ref, seconds, max_threads=16):
+    """The same single-threaded oracle run on row-partitioned slices of one call
+    (contiguous groups of requests) in host threads; the C calls release the
+    GIL.  Checks that the pieces reproduce the whole-call result.  Only for
+    single-call workloads with packed rows."""
+    import concurrent.futures as cf
+    import oracle
+    if w.blocks != 1 or w.row_offsets is not None or w.num_requests < 2:
+        return None
+    threads = max(1, min(max_threads, os.cpu_count() or 1, w.num_requests))
+    rows_of = w.block_lens.astype(np.int64) + 1
+    starts = np.concatenate([[0], np.cumsum(rows_of)])
+    bounds = np.linspace(0, w.num_requests, threads + 1).astype(int)
+
+    def piece(k):
+        i0, i1 = bounds[k], bounds[k + 1]
+        r0, r1 = starts[i0], starts[i1]
+        return oracle.verify(w.logits[r0:r1], w.draft_tokens[r0:r1], w.block_lens[i0:i1],
+                             w.tau[i0:i1], w.exc_cap[i0:i1], w.budget[i0:i1])
+
+    times = []
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        while True:
+            c0 = time.perf_counter()
+            parts = list(ex.map(piece, range(threads)))
+            times.append(time.perf_counter() - c0)
+            if sum(times) >= seconds / 4 or len(times) >= 5:
+                break
+    acc = np.concatenate([p["accept_len"] for p in parts])
+    nxt = np.concatenate([p["next_token"] for p in parts])
+    bud = np.concatenate([p["budget"] for p in parts])
+    same = (np.array_equal(acc, ref[0][0]) and np.array_equal(nxt, ref[1][0]) and
+            np.array_equal(bud.view(np.uint32), ref[2].view(np.uint32)))
+    med = statistics.median(times)
+    return {"value": w.rows_per_call / med, "unit": "rows/s", "cores": threads, "kind": "oracle",
+            "sample": "one full step split into %d row-contiguous request groups, each verified "
+                      "by the single-threaded C oracle in its own host thread; median of %d "
+                      "runs %.2fs; pieces equal the whole-call result: %s" % (
+                          threads, len(times), med, same)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -397,6 +452,75 @@ def main():
                             "the verifier's row pass alone"}
         log("row kernel alone: %.1f us, %.0f GB/s" % (row_ms * 1e3, row_only["achieved"]))
 
+    def timed_calls(fn, count, evict_first):
+        """Durations (ms) of `count` calls of fn, each between its own HIP events;
+        with evict_first, after a 512 MiB read-modify-write outside the events."""
+        evict = torch.zeros(2 * LLC_BYTES, dtype=torch.uint8, device=dev) if evict_first else None
+        spans = []
+        for _ in range(count):
+            if evict is not None:
+                evict.add_(1)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            spans.append((e0, e1))
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in spans]
+
+    # Per-call spread: a second pass of the same calls, each between its own events.
+    per_call = None
+    if not args.graph:
+        d = timed_calls(step, args.steps, cold)
+        per_call = {"median_ms": statistics.median(d), "min_ms": min(d), "max_ms": max(d),
+                    "calls": len(d), "cold": cold}
+
+    # Practical read ceiling: the row pass's access pattern with no ranking work
+    # (asd_read_probe) over the same logits.
+    practical = None
+    row_bytes_v = w.vocab * logits.element_size() if args.shards == 0 else 0
+    if (args.shards == 0 and w.blocks == 1 and row_bytes_v % 16 == 0
+            and logits.data_ptr() % 16 == 0):
+        out_word = torch.zeros(1, dtype=torch.int32, device=dev)
+        probe = lambda: asd.asd_read_probe(logits, w.rows_per_call, row_bytes_v, out_word)
+        for _ in range(3):
+            probe()
+        d = timed_calls(probe, args.steps, cold)
+        p_ms = statistics.mean(d)
+        practical = {"kernel": "asd_read_probe (the row pass's loads, no ranking)",
+                     "avg_launch_ms": p_ms, "bytes_per_launch": w.logit_bytes_per_call,
+                     "achieved": w.logit_bytes_per_call / (p_ms / 1e3) / 1e9,
+                     "frac": w.logit_bytes_per_call / (p_ms / 1e3) / 1e9 / PEAK_HBM_GBPS}
+        if row_only is not None:
+            practical["row_kernel_time_over_probe"] = row_only["avg_launch_ms"] / p_ms
+        log("read probe: %.1f us, %.0f GB/s" % (p_ms * 1e3, practical["achieved"]))
+
+    # Strict (B = 0) and ASD calls alternated on the same rows: the ASD scan's
+    # cost over exact greedy verification.
+    strict_vs_asd = None
+    if args.shards == 0 and not args.graph and not args.opportunity and w.blocks == 1:
+        strict_budget = pristine.clone()
+        strict_budget[:, 0] = 0.0
+        asd_budget = pristine.clone()
+        lg, dr, a, x = calls[0]
+        t_strict, t_asd = [], []
+        for i in range(2 * min(args.steps, 20)):
+            bud = strict_budget if i % 2 == 0 else asd_budget
+            if i % 2 == 1:
+                asd_budget.copy_(pristine)
+            d = timed_calls(lambda: asd.asd_verify(lg, dr, lens, tau, cap, bud, out_accept_len=a,
+                                                   out_next_token=x), 1, cold)
+            (t_strict if i % 2 == 0 else t_asd).append(d[0])
+        strict_vs_asd = {"strict_median_ms": statistics.median(t_strict),
+                         "asd_median_ms": statistics.median(t_asd),
+                         "asd_minus_strict_us": (statistics.median(t_asd) -
+                                                 statistics.median(t_strict)) * 1e3,
+                         "pairs": len(t_asd)}
+        log("strict %.1f us, asd %.1f us per call (medians of %d alternating pairs)" % (
+            strict_vs_asd["strict_median_ms"] * 1e3, strict_vs_asd["asd_median_ms"] * 1e3,
+            len(t_asd)))
+
     acceptance = None
     if args.shards == 0 and not args.graph:
         acceptance = acceptance_diagnostics(asd, torch, w, calls, lens, tau, cap, pristine)
@@ -421,6 +545,7 @@ def main():
     # Oracle: parity reference and CPU baseline (single-threaded, as written).
     parity = "not checked"
     cpu = None
+    cpu_threads = None
     if not args.no_cpu_baseline:
         import oracle
         def oracle_step():
@@ -464,6 +589,7 @@ def main():
                          "single-threaded C oracle, median %.2fs" % (
                              rows_step, w.vocab, w.dtype, len(times), med)}
         log("oracle: %.2fs per call (median of %d), parity %s" % (med, len(times), parity))
+        cpu_threads = threaded_oracle(w, ref, args.cpu_seconds)
 
     tag = workload_tag(args.config, w)
     kdesc = {1: "8", 2: "16", 3: "16", 4: "32", 5: "1to8"}[args.config]
@@ -540,8 +666,13 @@ def main():
         "torch_amax_same_logits_GBps": probe_gbps,
         "kernel_source_sha256_16": kernel_source_hash(),
     }
+    out["per_call"] = per_call
+    out["practical_read"] = practical
+    out["strict_vs_asd"] = strict_vs_asd
     if cpu is not None:
         out["cpu_baseline"] = cpu
+        out["cpu_baseline_threads"] = cpu_threads
+        out["host"] = host_info()
     print(json.dumps(out), flush=True)
 
 

@@ -371,6 +371,24 @@ asd_status asd_lmhead_verify(const void *hidden, const void *weight, int64_t d, 
                              int32_t *out_accept_len, int32_t *out_next_token,
                              int32_t *out_argmax, float *out_regret, void *stream);
 
+/*
+ * asd_read_probe -- a measurement helper: stream `rows` rows of `row_bytes`
+ * bytes from `buf` once, with the access pattern of the verifier's row pass
+ * (one 256-thread workgroup per row, 16-byte non-temporal loads, four per lane
+ * in flight) and no ranking work.  Its duration is the practical read ceiling
+ * that the row pass's bandwidth is compared with.
+ *
+ * buf             device memory, 16-byte aligned, rows * row_bytes bytes.
+ * rows            1 <= rows < 2^31.
+ * row_bytes       a multiple of 16, >= 16.
+ * out_word        device uint32: written only by a lane whose XOR of the words
+ *                 it read equals 0x9e3779b9 (so the loads cannot be elided; a
+ *                 caller can plant that value to check that the data is read).
+ * Allocates nothing; asynchronous on `stream`.
+ */
+asd_status asd_read_probe(const void *buf, int64_t rows, int64_t row_bytes, uint32_t *out_word,
+                          void *stream);
+
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 

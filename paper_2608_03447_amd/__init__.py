@@ -15,9 +15,10 @@ from .build import LIBRARY
 
 __all__ = ["asd_verify", "asd_verify_ws", "asd_verify_ex", "asd_shard_argmax",
            "asd_verify_partials", "asd_opportunity", "asd_commit", "asd_verify_commit",
-           "asd_lmhead_verify", "asd_device_error", "asd_workspace_bytes", "asd_status_string",
-           "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16", "ASD_GATE_RAW",
-           "ASD_DEVERR_NEGATIVE_K", "ASD_DEVERR_ROWS", "ASD_DEVERR_COMMIT", "library_path"]
+           "asd_lmhead_verify", "asd_device_error", "asd_read_probe", "asd_workspace_bytes",
+           "asd_status_string", "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16",
+           "ASD_GATE_RAW", "ASD_DEVERR_NEGATIVE_K", "ASD_DEVERR_ROWS", "ASD_DEVERR_COMMIT",
+           "library_path"]
 
 ASD_F32 = 0
 ASD_BF16 = 1
@@ -58,6 +59,8 @@ def _load():
     lib.asd_verify_ex.restype = ctypes.c_int
     lib.asd_device_error.argtypes = [vp, i32, vp]
     lib.asd_device_error.restype = ctypes.c_int
+    lib.asd_read_probe.argtypes = [vp, i64, i64, vp, vp]
+    lib.asd_read_probe.restype = ctypes.c_int
     lib.asd_shard_argmax.argtypes = [vp, ctypes.c_int, i64, i64, i64, i64, vp, vp, vp]
     lib.asd_shard_argmax.restype = ctypes.c_int
     lib.asd_verify_partials.argtypes = [vp, i32, i64, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp,
@@ -245,6 +248,23 @@ def asd_device_error(clear=False, device=None) -> int:
     if st != 0:
         raise AsdError(st, "asd_device_error")
     return int(word.value)
+
+
+def asd_read_probe(buf, rows, row_bytes, out_word):
+    """Stream ``rows`` x ``row_bytes`` of ``buf`` (a contiguous GPU tensor) with the
+    row pass's access pattern (``asd_read_probe``); ``out_word`` is a uint32-sized
+    int32 tensor on the same device."""
+    if (not buf.is_cuda or not buf.is_contiguous()
+            or buf.numel() * buf.element_size() < rows * row_bytes):
+        raise ValueError("buf must be a contiguous GPU tensor of at least rows * row_bytes bytes")
+    if out_word.dtype != torch.int32 or out_word.numel() < 1 or out_word.device != buf.device:
+        raise ValueError("out_word must be an int32 tensor on the buffer's device")
+    with torch.cuda.device(buf.device):
+        stream = torch.cuda.current_stream(buf.device).cuda_stream
+        st = _load().asd_read_probe(ctypes.c_void_p(buf.data_ptr()), int(rows), int(row_bytes),
+                                    ctypes.c_void_p(out_word.data_ptr()), ctypes.c_void_p(stream))
+    if st != 0:
+        raise AsdError(st, "asd_read_probe")
 
 
 def asd_shard_argmax(shard_logits, vocab_offset, vocab, draft_tokens, out_partials=None):

@@ -492,6 +492,17 @@ asd_status asd_lmhead_verify(const void* hidden, const void* weight, int64_t d, 
                : ASD_EHIP;
 }
 
+asd_status asd_read_probe(const void* buf, int64_t rows, int64_t row_bytes, uint32_t* out_word,
+                          void* stream) {
+    if (!buf || !out_word || ((uintptr_t)buf & 15) != 0) return ASD_EINVAL;
+    if (rows < 1 || rows >= ((int64_t)1 << 31) || row_bytes < 16 || row_bytes % 16 != 0 ||
+        row_bytes > INT64_MAX / rows)
+        return ASD_EINVAL;
+    return launch_read_probe(buf, rows, row_bytes, out_word, (hipStream_t)stream) == hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
 const char* asd_status_string(asd_status status) {
     switch (status) {
         case ASD_OK: return "ASD_OK";

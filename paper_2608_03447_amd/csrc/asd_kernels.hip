@@ -130,7 +130,7 @@ __device__ __forceinline__ uint32_t dword_keys(uint32_t w) {
         if constexpr (EB == 2) return bf16x2_keys(w);
         else return (int32_t)w < 0 ? 0x80000000u - w : w;
     } else {
-        if constexpr (EB == 2) return pkminu16(w & 0x7fff7fffu, 0x7f817f81u);
+        if constexpr (EB == 2) return pkminu16(w & 0x7fff7fffu, (uint32_t)KeyTraits<2>::kNan * 0x10001u);
         else return min(w & 0x7fffffffu, (uint32_t)KeyTraits<4>::kNan);
     }
 }
@@ -335,19 +335,44 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) saved[u] = (u32x4)(0u);
 
-    for (int64_t g = 0; g < nfull; ++g) {
+    // Full groups through two register buffers in ping-pong: a group's four
+    // loads are issued before the previous group is ranked, so each wavefront
+    // keeps eight 16-byte loads per lane in flight while it computes.  The
+    // scheduling barriers keep the compiler from moving ranking work (and its
+    // waits) ahead of the loads.
+    auto load_group = [&](u32x4 (&r)[kUnroll], int64_t g) {
         const u32x4* p = vec + v0 + g * kGroupVecs + tid;
-        u32x4 raw[kUnroll];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) raw[u] = __builtin_nontemporal_load(p + u * kRowThreads);
-        // All of the group's loads issue before any of them is waited for.
-        __builtin_amdgcn_sched_barrier(0);
-        const int32_t gk = group_max_key<EB, kMode, false>(raw, kUnroll, umax);
+        for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(p + u * kRowThreads);
+    };
+    auto rank_group = [&](const u32x4 (&r)[kUnroll], int64_t g) {
+        const int32_t gk = group_max_key<EB, kMode, false>(r, kUnroll, umax);
         const bool better = gk > best_key;
         best_key = better ? gk : best_key;
         best_group = better ? g : best_group;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) saved[u] = better ? raw[u] : saved[u];
+        for (int u = 0; u < kUnroll; ++u) saved[u] = better ? r[u] : saved[u];
+    };
+    if (nfull > 0) {
+        u32x4 ra[kUnroll], rb[kUnroll];
+        load_group(ra, 0);
+        int64_t g = 0;
+        for (; g + 2 < nfull; g += 2) {
+            load_group(rb, g + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            rank_group(ra, g);
+            load_group(ra, g + 2);
+            __builtin_amdgcn_sched_barrier(0);
+            rank_group(rb, g + 1);
+        }
+        if (g + 1 < nfull) {
+            load_group(rb, g + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            rank_group(ra, g);
+            rank_group(rb, g + 1);
+        } else {
+            rank_group(ra, g);
+        }
     }
     best_nvalid = best_group >= 0 ? kUnroll : 0;
 
@@ -424,14 +449,14 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
 
 // ----------------------------------------------------------- stage 1 kernel
 
-template <int EB>
-//
 // `logits` rows hold columns [col_offset, col_offset + vocab) of the full
 // vocabulary (col_offset = 0 and vocab = V unless the rows are one tensor-
 // parallel shard); columns are reported globally.  With `partials` set every
 // tile writes a partial (split rows, or one shard of each row); otherwise each
-// row is one tile and writes its record.
-__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(8))) void asd_row_kernel(
+// row is one tile and writes its record.  Six wavefronts per SIMD: the two load
+// buffers fit in 80 VGPRs with no spill (a tighter budget spills).
+template <int EB>
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(6))) void asd_row_kernel(
     const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
     int64_t chunk_vecs, const int32_t* __restrict__ draft_tokens,
     TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
@@ -1181,6 +1206,37 @@ __global__ void asd_fill_u64_kernel(unsigned long long* p, int64_t n, unsigned l
     if (i < n) p[i] = v;
 }
 
+// ------------------------------------------------------- read probe
+//
+// The row kernel's access pattern with no ranking: one workgroup per row,
+// groups of four 16-byte non-temporal loads per lane issued before any wait,
+// each vector folded into a per-lane XOR.  Its duration is the practical read
+// ceiling of that pattern.  A lane whose fold equals kProbeMark stores it to
+// *out (keeps the loads live; callers can plant the mark to check the read).
+constexpr uint32_t kProbeMark = 0x9e3779b9u;
+
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(8))) void
+asd_read_probe_kernel(const unsigned char* __restrict__ buf, int64_t row_bytes,
+                      uint32_t* __restrict__ out) {
+    const u32x4* vec = (const u32x4*)(buf + (int64_t)blockIdx.x * row_bytes);
+    const int64_t nvec = row_bytes / 16;
+    uint32_t acc = 0;
+    int64_t i = threadIdx.x;
+    for (; i + (kUnroll - 1) * kRowThreads < nvec; i += kGroupVecs) {
+        u32x4 r[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(vec + i + u * kRowThreads);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) acc ^= r[u].x ^ r[u].y ^ r[u].z ^ r[u].w;
+    }
+    for (; i < nvec; i += kRowThreads) {
+        const u32x4 v = __builtin_nontemporal_load(vec + i);
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == kProbeMark) *out = acc;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launch
@@ -1301,6 +1357,13 @@ hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t 
     A.row_best = best;
     A.row_draft_bits = draft_bits;
     return launch_scan(A, true, stream);
+}
+
+hipError_t launch_read_probe(const void* buf, int64_t rows, int64_t row_bytes, uint32_t* out,
+                             hipStream_t stream) {
+    asd_read_probe_kernel<<<(unsigned)rows, kRowThreads, 0, stream>>>(
+        (const unsigned char*)buf, row_bytes, out);
+    return hipGetLastError();
 }
 
 }  // namespace asd

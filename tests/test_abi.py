@@ -308,3 +308,15 @@ def test_device_error_needs_an_output():
     assert lib.asd_device_error(None, 0, None) == 1
     assert asd.ASD_GATE_RAW == 1
     assert (asd.ASD_DEVERR_NEGATIVE_K, asd.ASD_DEVERR_ROWS, asd.ASD_DEVERR_COMMIT) == (1, 2, 4)
+
+
+@pytest.mark.parametrize("args", [
+    (None, 1, 16, 0x2000), (0x1008, 1, 16, 0x2000), (0x1000, 0, 16, 0x2000),
+    (0x1000, 1 << 31, 16, 0x2000), (0x1000, 1, 8, 0x2000), (0x1000, 1, 24, 0x2000),
+    (0x1000, 1, 16, None), (0x1000, 1 << 30, 1 << 62, 0x2000),
+])
+def test_read_probe_rejects_invalid_arguments(args):
+    lib = asd._load()
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    buf, rows, row_bytes, out = args
+    assert lib.asd_read_probe(vp(buf), rows, row_bytes, vp(out), None) == 1

@@ -95,3 +95,19 @@ def test_workload_tag_names_the_shape():
     assert bench.workload_tag(3, Wk) == "b256_k16_v151936_bf16"
     Wk.blocks = 64
     assert bench.workload_tag(1, Wk).endswith("_seq64")
+
+
+def test_threaded_oracle_pieces_reproduce_the_whole_call():
+    import workloads as W
+    for cfg in (3, 5):
+        w = W.make_config(cfg, batch=24, vocab=3000)
+        ref = oracle.verify(w.logits, w.draft_tokens, w.block_lens, w.tau, w.exc_cap, w.budget)
+        whole = (ref["accept_len"][None], ref["next_token"][None], ref["budget"])
+        got = bench.threaded_oracle(w, whole, 0.01, max_threads=4)
+        assert got["kind"] == "oracle" and 1 <= got["cores"] <= 4 and got["value"] > 0
+        assert got["sample"].endswith("True")
+
+
+def test_host_info_reports_cpu_count():
+    info = bench.host_info()
+    assert info["nproc"] == os.cpu_count()
