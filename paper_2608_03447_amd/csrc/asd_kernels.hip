@@ -181,17 +181,15 @@ __device__ __forceinline__ int32_t key_of(uint32_t pattern) {
     else return (int32_t)dword_keys<4, kMode>(pattern);
 }
 
-// Element e of a 16-byte vector as (key, binary32 bits).
+// Greatest key among the elements of one dword (two bf16 or one f32).
 template <int EB, int kMode>
-__device__ __forceinline__ void element_of(const u32x4& v, int e, int32_t& key, uint32_t& bits) {
+__device__ __forceinline__ int32_t dword_max_key(uint32_t w) {
+    const uint32_t k = dword_keys<EB, kMode>(w);
     if constexpr (EB == 2) {
-        const uint32_t w = v[e >> 1];
-        const uint32_t h = (e & 1) ? (w >> 16) : (w & 0xffffu);
-        key = key_of<2, kMode>(h);
-        bits = h << 16;
+        const int32_t lo = (int32_t)(int16_t)(k & 0xffffu), hi = (int32_t)k >> 16;
+        return lo > hi ? lo : hi;
     } else {
-        bits = v[e];
-        key = key_of<4, kMode>(bits);
+        return (int32_t)k;
     }
 }
 
@@ -399,26 +397,45 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
         }
     }
 
-    // this lane's first element holding best_key
+    // This lane's first element holding best_key, narrowed level by level in
+    // column order: the first vector of the saved group whose greatest key is
+    // best_key, then that vector's first such dword, then (bf16) the half.
     packed = pack_kc(KeyTraits<4>::kNone, 0x7fffffff);
     bits = 0;
     if (best_group >= 0) {
-        bool found = false;
+        int su = 0;
+        u32x4 sv = saved[0];
+        bool hit = false;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-#pragma unroll
-            for (int e = 0; e < kEpv; ++e) {
-                int32_t k;
-                uint32_t b;
-                element_of<EB, kMode>(saved[u], e, k, b);
-                if (!found && u < best_nvalid && k == best_key) {
-                    found = true;
-                    const int64_t vi = v0 + best_group * kGroupVecs + u * kRowThreads + tid;
-                    packed = pack_kc(k, col_offset + geom.head + vi * kEpv + e);
-                    bits = b;
-                }
-            }
+            const int32_t mk = max(max(dword_max_key<EB, kMode>(saved[u].x),
+                                       dword_max_key<EB, kMode>(saved[u].y)),
+                                   max(dword_max_key<EB, kMode>(saved[u].z),
+                                       dword_max_key<EB, kMode>(saved[u].w)));
+            const bool take = !hit && u < best_nvalid && mk == best_key;
+            su = take ? u : su;
+            sv = take ? saved[u] : sv;
+            hit = hit || take;
         }
+        int d = 3;
+        uint32_t w = sv.w;
+#pragma unroll
+        for (int j = 2; j >= 0; --j) {             // the first dword holding best_key wins
+            const bool take = dword_max_key<EB, kMode>(sv[j]) == best_key;
+            d = take ? j : d;
+            w = take ? sv[j] : w;
+        }
+        int e;
+        if constexpr (EB == 2) {
+            const bool low = key_of<2, kMode>(w & 0xffffu) == best_key;
+            e = 2 * d + (low ? 0 : 1);
+            bits = (low ? (w & 0xffffu) : (w >> 16)) << 16;
+        } else {
+            e = d;
+            bits = w;
+        }
+        const int64_t vi = v0 + best_group * kGroupVecs + su * kRowThreads + tid;
+        packed = pack_kc(best_key, col_offset + geom.head + vi * kEpv + e);
     }
 
     if constexpr (kMode == kKeysRaw) {
