@@ -619,6 +619,8 @@ def main():
         roofline = {"kernel": "asd_row_kernel", "bound": "hbm", "achieved": row_only["achieved"],
                     "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": row_only["frac"],
                     "traffic": traffic,
+                    "traffic_GBps": (traffic / (row_only["avg_launch_ms"] / 1e3) / 1e9
+                                     if traffic else None),
                     "algorithmic_bytes_per_launch": row_only["algorithmic_bytes_per_launch"],
                     "avg_launch_ms": row_only["avg_launch_ms"], "timing": row_only["note"]}
     else:
