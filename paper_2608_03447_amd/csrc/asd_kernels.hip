@@ -61,8 +61,7 @@ constexpr int kWaves = kRowThreads / 64;
 // with the sign bit set (-inf's).
 template <int EB> struct KeyTraits;
 template <> struct KeyTraits<2> {
-    static constexpr int32_t kNone = -0x8000;         // bf16 keys lie in [-0x7f80, 0x7f81]
-    static constexpr uint32_t kNonePacked = 0x80008000u;
+    static constexpr uint32_t kNonePacked = 0x80008000u;   // bf16 keys lie in [-0x7f80, 0x7f81]
     static constexpr int32_t kInf = 0x7f80;
     static constexpr int32_t kNan = 0x7f81;
     static constexpr uint32_t kNegInfPattern = 0xff80u;
@@ -81,21 +80,21 @@ __device__ __forceinline__ int32_t f32_key(uint32_t u) {
     return mag > 0x7f800000u ? KeyTraits<4>::kNan : key;
 }
 
-// Three ways to rank the logits of a row tile, cheapest first.
+// Three ways to rank logits, cheapest first.
 //  kKeysRaw:   the raw bit patterns read as signed integers.  For every pattern
 //              with the sign bit clear that is neither +0 nor a NaN this equals
 //              the key, and every pattern with the sign bit set reads as
-//              negative.  So when the tile holds a pattern in [1, +inf] and no
-//              NaN, the raw maximum is the exact maximum, found with one
-//              integer max per element.  The raw pass also keeps the greatest
-//              pattern read as unsigned, which exceeds -inf's exactly when a
-//              NaN with the sign bit set is present (a NaN with it clear shows
-//              in the raw maximum).
-//  kKeysExact: sign-magnitude keys, exact for every number (tiles whose raw
-//              maximum is below 1 and that hold no NaN).
+//              negative.  So among elements that include a number in [1, +inf]
+//              and no NaN, the raw maximum is the exact maximum, found with one
+//              integer max per element.
+//  kKeysExact: sign-magnitude keys, exact for every number.
 //  kKeysNan:   min(magnitude, kNan): every NaN gets kNan and every number a
 //              smaller key, so in a tile known to hold a NaN the greatest key
 //              is kNan and its first element is the tile's first NaN.
+// With raw and sign-magnitude keys a NaN's key is not kNan.  Those passes keep
+// the greatest pattern read as unsigned, which exceeds -inf's exactly when a
+// NaN with the sign bit set is present; a NaN with it clear shows as a greatest
+// key above +inf's.  Either sends the tile to a NaN pass.
 constexpr int kKeysRaw = 0, kKeysExact = 1, kKeysNan = 2;
 constexpr int32_t kRawExactFrom = 1;
 
@@ -150,7 +149,7 @@ __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], in
             uint32_t m = pkmax16(pkmax16(k0, k1), pkmax16(k2, k3));
             if (kMasked && u >= nvalid) m = KeyTraits<2>::kNonePacked;
             acc = pkmax16(acc, m);
-            if constexpr (kMode == kKeysRaw)
+            if constexpr (kMode != kKeysNan)
                 umax = pkmaxu16(umax, pkmaxu16(pkmaxu16(raw[u].x, raw[u].y),
                                                pkmaxu16(raw[u].z, raw[u].w)));
         }
@@ -167,7 +166,7 @@ __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], in
                                 (int32_t)dword_keys<4, kMode>(raw[u].w)));
             if (kMasked && u >= nvalid) m = KeyTraits<4>::kNone;
             acc = max(acc, m);
-            if constexpr (kMode == kKeysRaw)
+            if constexpr (kMode != kKeysNan)
                 umax = max(umax, max(max(raw[u].x, raw[u].y), max(raw[u].z, raw[u].w)));
         }
         return acc;
@@ -305,66 +304,122 @@ __device__ void write_packed_offsets(int32_t num_requests, const int32_t* __rest
     }
 }
 
-// One lane's best (key, column) and bits over its share of a tile: the
-// tile's 16-byte vectors [split * chunk_vecs, ...) of the row's aligned middle,
-// plus the row's unaligned head (split 0) and tail (last split) elements.  In
-// the raw pass `nan_seen` tells whether the lane's share holds a NaN that the
-// raw maximum does not show (one with the sign bit set, or any NaN among the
-// head and tail elements); the other passes leave it alone.
-template <int EB, int kMode>
-__device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const RowGeom& geom,
-                                          int64_t vocab, int64_t col_offset, int split,
-                                          int splits, int64_t chunk_vecs, int tid,
-                                          unsigned long long& packed, uint32_t& bits,
-                                          bool& nan_seen) {
-    constexpr int kEpv = 16 / EB;
-    // stream this tile's 16-byte vectors
-    const u32x4* vec = (const u32x4*)(row_ptr + geom.head * EB);
-    const int64_t v0 = (int64_t)split * chunk_vecs;
-    const int64_t v1 = min(v0 + chunk_vecs, geom.nvec);
-    const int64_t nv = v1 > v0 ? v1 - v0 : 0;
-    const int64_t nfull = nv / kGroupVecs;
+// Where one lane's share of a tile lies: 16-byte vectors [v0, v1) of the row's
+// aligned middle, nfull whole groups of kGroupVecs vectors, then a partial one.
+struct TileSpan {
+    const u32x4* vec;
+    int32_t v0, v1, nv, nfull;    // vector counts: a row has fewer than 2^28 vectors
+    int tid;
+};
 
-    int32_t best_key = kMode == kKeysRaw ? KeyTraits<4>::kNone : KeyTraits<EB>::kNone;
-    int64_t best_group = -1;
-    int best_nvalid = 0;
-    uint32_t umax = 0;
+__device__ __forceinline__ void load_group(const TileSpan& t, u32x4 (&r)[kUnroll], int32_t g) {
+    const u32x4* p = t.vec + t.v0 + g * kGroupVecs + t.tid;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(p + u * kRowThreads);
+}
+
+// The lane's first element holding `key` in a saved group, narrowed level by
+// level in column order: the first vector whose greatest key is `key`, then
+// that vector's first such dword, then (bf16) the half.  Returns the element's
+// index within the group's vectors' elements and its binary32 bits.
+template <int EB, int kMode>
+__device__ __forceinline__ void find_first(const u32x4 (&saved)[kUnroll], int nvalid, int32_t key,
+                                           int& su, int& e, uint32_t& bits) {
+    su = 0;
+    u32x4 sv = saved[0];
+    bool hit = false;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const int32_t mk = max(max(dword_max_key<EB, kMode>(saved[u].x),
+                                   dword_max_key<EB, kMode>(saved[u].y)),
+                               max(dword_max_key<EB, kMode>(saved[u].z),
+                                   dword_max_key<EB, kMode>(saved[u].w)));
+        const bool take = !hit && u < nvalid && mk == key;
+        su = take ? u : su;
+        sv = take ? saved[u] : sv;
+        hit = hit || take;
+    }
+    int d = 3;
+    uint32_t w = sv.w;
+#pragma unroll
+    for (int j = 2; j >= 0; --j) {                 // the first dword holding key wins
+        const bool take = dword_max_key<EB, kMode>(sv[j]) == key;
+        d = take ? j : d;
+        w = take ? sv[j] : w;
+    }
+    if constexpr (EB == 2) {
+        const bool low = key_of<2, kMode>(w & 0xffffu) == key;
+        e = 2 * d + (low ? 0 : 1);
+        bits = (low ? (w & 0xffffu) : (w >> 16)) << 16;
+    } else {
+        e = d;
+        bits = w;
+    }
+}
+
+// Key modes of rank_share beyond the three key kinds: choose raw or
+// sign-magnitude keys from the first whole group (see tile_best).
+constexpr int kKeysChoose = 3;
+
+// One lane's ranking of its share of a tile: the greatest key, the first
+// element holding it (as a packed (key, column)) and that element's binary32
+// bits.  `mode` is uniform across the wavefront; the loop is shared and each
+// group's ranking branches on it.  With kKeysChoose the wavefront ranks its
+// first whole group with raw keys and keeps them if that group holds a number
+// in [1, +inf] in any lane, else switches to sign-magnitude keys (ranking the
+// group again from its registers).  Except with NaN keys, `umax` takes the
+// greatest pattern read as unsigned (per 16-bit half for bf16).
+template <int EB>
+__device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t col_base,
+                                           unsigned long long& packed, uint32_t& bits,
+                                           uint32_t& umax) {
+    constexpr int kEpv = 16 / EB;
+    int32_t best_key = KeyTraits<4>::kNone;
+    int32_t best_group = -1;
     u32x4 saved[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) saved[u] = (u32x4)(0u);
 
-    // Full groups through two register buffers in ping-pong: a group's four
-    // loads are issued before the previous group is ranked, so each wavefront
-    // keeps eight 16-byte loads per lane in flight while it computes.  The
-    // scheduling barriers keep the compiler from moving ranking work (and its
-    // waits) ahead of the loads.
-    auto load_group = [&](u32x4 (&r)[kUnroll], int64_t g) {
-        const u32x4* p = vec + v0 + g * kGroupVecs + tid;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(p + u * kRowThreads);
-    };
-    auto rank_group = [&](const u32x4 (&r)[kUnroll], int64_t g) {
-        const int32_t gk = group_max_key<EB, kMode, false>(r, kUnroll, umax);
+    auto rank_group = [&](const u32x4 (&r)[kUnroll], int32_t g) {
+        int32_t gk;
+        if (mode == kKeysNan) {
+            gk = group_max_key<EB, kKeysNan, false>(r, kUnroll, umax);
+        } else if (mode == kKeysExact) {
+            gk = group_max_key<EB, kKeysExact, false>(r, kUnroll, umax);
+        } else {
+            gk = group_max_key<EB, kKeysRaw, false>(r, kUnroll, umax);
+            if (mode == kKeysChoose) {
+                const int raw_ok =
+                    __ballot(gk >= kRawExactFrom && gk <= KeyTraits<EB>::kInf) != 0ull;
+                mode = __builtin_amdgcn_readfirstlane(raw_ok) ? kKeysRaw : kKeysExact;
+                if (mode == kKeysExact) gk = group_max_key<EB, kKeysExact, false>(r, kUnroll, umax);
+            }
+        }
         const bool better = gk > best_key;
         best_key = better ? gk : best_key;
         best_group = better ? g : best_group;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) saved[u] = better ? r[u] : saved[u];
     };
-    if (nfull > 0) {
+    // Whole groups through two register buffers in ping-pong: a group's four
+    // loads are issued before the previous group is ranked, so each wavefront
+    // keeps eight 16-byte loads per lane in flight while it computes.  The
+    // scheduling barriers keep the compiler from moving ranking work (and its
+    // waits) ahead of the loads.
+    if (t.nfull > 0) {
         u32x4 ra[kUnroll], rb[kUnroll];
-        load_group(ra, 0);
-        int64_t g = 0;
-        for (; g + 2 < nfull; g += 2) {
-            load_group(rb, g + 1);
+        load_group(t, ra, 0);
+        int32_t g = 0;
+        for (; g + 2 < t.nfull; g += 2) {
+            load_group(t, rb, g + 1);
             __builtin_amdgcn_sched_barrier(0);
             rank_group(ra, g);
-            load_group(ra, g + 2);
+            load_group(t, ra, g + 2);
             __builtin_amdgcn_sched_barrier(0);
             rank_group(rb, g + 1);
         }
-        if (g + 1 < nfull) {
-            load_group(rb, g + 1);
+        if (g + 1 < t.nfull) {
+            load_group(t, rb, g + 1);
             __builtin_amdgcn_sched_barrier(0);
             rank_group(ra, g);
             rank_group(rb, g + 1);
@@ -372,73 +427,80 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
             rank_group(ra, g);
         }
     }
-    best_nvalid = best_group >= 0 ? kUnroll : 0;
+    if (mode == kKeysChoose) mode = kKeysExact;      // no whole group: sign-magnitude keys
+    int best_nvalid = best_group >= 0 ? kUnroll : 0;
 
-    if (nv > nfull * kGroupVecs) {       // the tile's last, partial group
-        const int64_t g = nfull;
-        const int64_t first = v0 + g * kGroupVecs + tid;
+    if (t.nv > t.nfull * kGroupVecs) {     // the tile's last, partial group
+        const int32_t first = t.v0 + t.nfull * kGroupVecs + t.tid;
         int nvalid = 0;
         u32x4 raw[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             raw[u] = (u32x4)(0u);
-            if (first + u * kRowThreads < v1) {
-                raw[u] = __builtin_nontemporal_load(vec + first + u * kRowThreads);
+            if (first + u * kRowThreads < t.v1) {
+                raw[u] = __builtin_nontemporal_load(t.vec + first + u * kRowThreads);
                 ++nvalid;
             }
         }
-        const int32_t gk = group_max_key<EB, kMode, true>(raw, nvalid, umax);
+        int32_t gk;
+        if (mode == kKeysRaw) gk = group_max_key<EB, kKeysRaw, true>(raw, nvalid, umax);
+        else if (mode == kKeysExact) gk = group_max_key<EB, kKeysExact, true>(raw, nvalid, umax);
+        else gk = group_max_key<EB, kKeysNan, true>(raw, nvalid, umax);
         if (nvalid > 0 && gk > best_key) {
             best_key = gk;
-            best_group = g;
+            best_group = t.nfull;
             best_nvalid = nvalid;
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) saved[u] = raw[u];
         }
     }
 
-    // This lane's first element holding best_key, narrowed level by level in
-    // column order: the first vector of the saved group whose greatest key is
-    // best_key, then that vector's first such dword, then (bf16) the half.
     packed = pack_kc(KeyTraits<4>::kNone, 0x7fffffff);
     bits = 0;
     if (best_group >= 0) {
-        int su = 0;
-        u32x4 sv = saved[0];
-        bool hit = false;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const int32_t mk = max(max(dword_max_key<EB, kMode>(saved[u].x),
-                                       dword_max_key<EB, kMode>(saved[u].y)),
-                                   max(dword_max_key<EB, kMode>(saved[u].z),
-                                       dword_max_key<EB, kMode>(saved[u].w)));
-            const bool take = !hit && u < best_nvalid && mk == best_key;
-            su = take ? u : su;
-            sv = take ? saved[u] : sv;
-            hit = hit || take;
-        }
-        int d = 3;
-        uint32_t w = sv.w;
-#pragma unroll
-        for (int j = 2; j >= 0; --j) {             // the first dword holding best_key wins
-            const bool take = dword_max_key<EB, kMode>(sv[j]) == best_key;
-            d = take ? j : d;
-            w = take ? sv[j] : w;
-        }
-        int e;
-        if constexpr (EB == 2) {
-            const bool low = key_of<2, kMode>(w & 0xffffu) == best_key;
-            e = 2 * d + (low ? 0 : 1);
-            bits = (low ? (w & 0xffffu) : (w >> 16)) << 16;
-        } else {
-            e = d;
-            bits = w;
-        }
-        const int64_t vi = v0 + best_group * kGroupVecs + su * kRowThreads + tid;
-        packed = pack_kc(best_key, col_offset + geom.head + vi * kEpv + e);
+        int su, e;
+        if (mode == kKeysRaw) find_first<EB, kKeysRaw>(saved, best_nvalid, best_key, su, e, bits);
+        else if (mode == kKeysExact)
+            find_first<EB, kKeysExact>(saved, best_nvalid, best_key, su, e, bits);
+        else find_first<EB, kKeysNan>(saved, best_nvalid, best_key, su, e, bits);
+        const int64_t vi = (int64_t)t.v0 + best_group * kGroupVecs + su * kRowThreads + t.tid;
+        packed = pack_kc(best_key, col_base + vi * kEpv + e);
     }
+}
 
-    if constexpr (kMode == kKeysRaw) {
+// One lane's best (key, column) and bits over its share of a tile: the
+// tile's 16-byte vectors [split * chunk_vecs, ...) of the row's aligned middle,
+// plus the row's unaligned head (split 0) and tail (last split) elements.
+//
+// kNanPass = false, the first pass.  Each wavefront ranks its first group with
+// raw keys; if that group holds a number in [1, +inf] in any lane, raw keys
+// rank the wavefront's whole share (every key that can win is then exact),
+// else sign-magnitude keys do.  So the tile's greatest key is exact unless the
+// tile holds a NaN, and `nan_seen` tells whether the lane's share holds one
+// that the greatest key does not show (one with the sign bit set, or any NaN
+// among the head and tail elements).
+// kNanPass = true: NaN keys, for a tile known to hold a NaN.
+template <int EB, bool kNanPass>
+__device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const RowGeom& geom,
+                                          int64_t vocab, int64_t col_offset, int split,
+                                          int splits, int64_t chunk_vecs, int tid,
+                                          unsigned long long& packed, uint32_t& bits,
+                                          bool& nan_seen) {
+    constexpr int kScalarMode = kNanPass ? kKeysNan : kKeysExact;
+    TileSpan t;
+    t.vec = (const u32x4*)(row_ptr + geom.head * EB);
+    t.v0 = (int32_t)(split * chunk_vecs);
+    t.v1 = (int32_t)min(split * chunk_vecs + chunk_vecs, geom.nvec);
+    t.nv = t.v1 > t.v0 ? t.v1 - t.v0 : 0;
+    t.nfull = t.nv / kGroupVecs;
+    t.tid = tid;
+    const int64_t col_base = col_offset + geom.head;
+
+    uint32_t umax = 0;
+    if constexpr (kNanPass) {
+        rank_share<EB>(t, kKeysNan, col_base, packed, bits, umax);
+    } else {
+        rank_share<EB>(t, kKeysChoose, col_base, packed, bits, umax);
         if constexpr (EB == 2)
             nan_seen = max(umax & 0xffffu, umax >> 16) > KeyTraits<2>::kNegInfPattern;
         else
@@ -449,19 +511,18 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
     if (split == 0 && tid < geom.head) {
         int32_t k;
         uint32_t b;
-        load_scalar<EB, kMode>(row_ptr + (int64_t)tid * EB, k, b);
+        load_scalar<EB, kScalarMode>(row_ptr + (int64_t)tid * EB, k, b);
         take_better(packed, bits, pack_kc(k, col_offset + tid), b);
-        if constexpr (kMode == kKeysRaw) nan_seen = nan_seen || (b & 0x7fffffffu) > 0x7f800000u;
+        if constexpr (!kNanPass) nan_seen = nan_seen || (b & 0x7fffffffu) > 0x7f800000u;
     }
     if (split == splits - 1 && tid < vocab - geom.tail) {
         const int64_t c = geom.tail + tid;
         int32_t k;
         uint32_t b;
-        load_scalar<EB, kMode>(row_ptr + c * EB, k, b);
+        load_scalar<EB, kScalarMode>(row_ptr + c * EB, k, b);
         take_better(packed, bits, pack_kc(k, col_offset + c), b);
-        if constexpr (kMode == kKeysRaw) nan_seen = nan_seen || (b & 0x7fffffffu) > 0x7f800000u;
+        if constexpr (!kNanPass) nan_seen = nan_seen || (b & 0x7fffffffu) > 0x7f800000u;
     }
-
 }
 
 // ----------------------------------------------------------- stage 1 kernel
@@ -502,34 +563,28 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(6))
         load_scalar<EB, kKeysRaw>(row_ptr + x_local * EB, k_unused, draft_bits);
     }
 
-    // ---- rank the tile by raw patterns.  If it holds a NaN, rank it again to
-    // find its first NaN; else if its raw maximum is below 1 (no positive
-    // number), rank it again with sign-magnitude keys.
+    // ---- rank the tile (first pass); if it holds a NaN, rank it again to find
+    // its first NaN.
     unsigned long long packed;
     uint32_t bits;
     bool nan_seen = false;
-    tile_best<EB, kKeysRaw>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
-                            packed, bits, nan_seen);
+    tile_best<EB, false>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid, packed,
+                         bits, nan_seen);
     __shared__ int s_nan[kWaves];
     const bool wave_nan = __ballot(nan_seen) != 0ull;
     if ((tid & 63) == 0) s_nan[tid >> 6] = wave_nan;
     block_reduce(packed, bits);          // its barrier also publishes s_nan
-    __shared__ int s_mode;
+    __shared__ int s_again;
     if (tid == 0) {
-        const int32_t k = packed_key(packed);
-        int any_nan = k > KeyTraits<EB>::kInf;
+        int any_nan = packed_key(packed) > KeyTraits<EB>::kInf;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) any_nan |= s_nan[w];
-        s_mode = any_nan ? kKeysNan : (k < kRawExactFrom ? kKeysExact : kKeysRaw);
+        s_again = any_nan;
     }
     __syncthreads();
-    if (s_mode == kKeysExact) {
-        tile_best<EB, kKeysExact>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs,
-                                  tid, packed, bits, nan_seen);
-        block_reduce(packed, bits);
-    } else if (s_mode == kKeysNan) {
-        tile_best<EB, kKeysNan>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
-                                packed, bits, nan_seen);
+    if (s_again) {
+        tile_best<EB, true>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
+                            packed, bits, nan_seen);
         block_reduce(packed, bits);
     }
     if (tid != 0) return;

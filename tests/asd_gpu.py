@@ -24,10 +24,8 @@ def gpu_verify(logits, draft, lens, tau, cap, budget, row_offsets=None, dev="cud
     tl = device_logits(logits, dev)
     td = torch.from_numpy(np.ascontiguousarray(draft, dtype=np.int32)).to(dev)
     tk = torch.from_numpy(np.ascontiguousarray(lens, dtype=np.int32)).to(dev)
-    tt = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(
-        np.asarray(tau, np.float32), (n,)))).to(dev)
-    tc = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(
-        np.asarray(cap, np.int32), (n,)))).to(dev)
+    tt = torch.from_numpy(np.array(np.broadcast_to(np.asarray(tau, np.float32), (n,)))).to(dev)
+    tc = torch.from_numpy(np.array(np.broadcast_to(np.asarray(cap, np.int32), (n,)))).to(dev)
     tb = torch.from_numpy(np.array(budget, dtype=np.float32).reshape(n, 2)).to(dev)
     to = None if row_offsets is None else torch.from_numpy(
         np.ascontiguousarray(row_offsets, dtype=np.int64)).to(dev)

@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 import workloads as W
 from asd_gpu import describe, gpu_verify, mismatches, oracle_verify
 
@@ -435,3 +436,44 @@ def test_sharded_packed_offsets_both_paths(num_requests):
     r = oracle_verify(logits, draft, lens, 2.0, 1, budget)
     bad = mismatches(g, r)
     assert not bad, "%d requests differ in %s: %s" % (num_requests, bad, describe(g, r))
+
+
+# ------------------------------------------------ per-wavefront key choice
+
+def _mixed_sign_blocks(rng, rows, vocab, block, dtype):
+    """Rows built from `block`-element runs that are either all negative or
+    mixed-sign, so that within one tile some wavefronts meet a positive number
+    in their first group and others do not; a few rows hold only negatives and
+    signed zeros (the maximum is then +-0 and the first zero wins)."""
+    z = -rng.uniform(0.25, 6.0, size=(rows, vocab)).astype(np.float32)
+    for r in range(rows):
+        kind = rng.integers(0, 4)
+        if kind == 0:                               # zeros only, both signs
+            cols = rng.integers(0, vocab, int(rng.integers(1, 6)))
+            z[r, cols] = rng.choice(np.array([0.0, -0.0], np.float32), cols.size)
+        elif kind == 1:                             # one negative maximum, tied twice
+            a, b = rng.integers(0, vocab, 2)
+            z[r, a] = z[r, b] = np.float32(-0.125)
+        else:                                       # positive runs here and there
+            for start in range(0, vocab, block):
+                if rng.random() < 0.15:
+                    n = min(block, vocab - start)
+                    z[r, start:start + n] = rng.normal(0, 2, n).astype(np.float32)
+            if kind == 3:                           # the maximum late in the row
+                z[r, int(rng.integers(vocab // 2, vocab))] = np.float32(30.0)
+    return W.f32_to_bf16(z) if dtype == "bf16" else z
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rows,vocab", [(300, 32768), (9, 151936), (40, 50001)])
+def test_wavefronts_choose_raw_or_sign_magnitude_keys(dtype, rows, vocab):
+    rng = np.random.default_rng(rows + vocab + (dtype == "f32"))
+    block = 512 if dtype == "bf16" else 256        # 64 lanes x one 16-byte vector
+    logits = _mixed_sign_blocks(rng, rows, vocab, block, dtype)
+    y = oracle.argmax_rows(logits)
+    draft = np.where(rng.random(rows) < 0.6, y, rng.integers(0, vocab, rows)).astype(np.int32)
+    K = 2 if rows % 3 == 0 else (rows // 3 if rows >= 3 else 0)
+    lens = np.full(rows // (K + 1), K, np.int32)
+    used = int(np.sum(lens + 1))
+    check(logits[:used], draft[:used], lens, 1.0, 2, [[4.0, 0.0]] * len(lens),
+          label="wave-modes-%s-%dx%d" % (dtype, rows, vocab))
