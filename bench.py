@@ -45,10 +45,16 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
+    """Hash of the library's sources with comments and whitespace removed, so that
+    an edit to a comment does not detach the counter profiles measured on the
+    same code."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -135,8 +135,9 @@ __device__ __forceinline__ uint32_t dword_keys(uint32_t w) {
 }
 
 // Max key over the 16-byte vectors of one group; vectors u >= nvalid are
-// ignored.  In the raw pass `umax` also takes the greatest pattern read as
-// unsigned (per 16-bit half for bf16); masked vectors hold zero and leave it.
+// ignored.  With raw and sign-magnitude keys `umax` also takes the greatest
+// pattern read as unsigned (per 16-bit half for bf16); masked vectors hold zero
+// and leave it.
 template <int EB, int kMode, bool kMasked>
 __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], int nvalid,
                                                  uint32_t& umax) {
