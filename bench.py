@@ -226,6 +226,9 @@ def main():
                          "2: 32 requests, K=16, V=151,936 bf16; 3 (default): 256 requests, K=16, "
                          "V=151,936 bf16; 4: 64 requests, K=32, V=151,936 f32; 5: 512 requests, "
                          "K=1..8, V=129,280 bf16")
+    ap.add_argument("--seed", type=int, default=None,
+                    help="seed of the synthetic workload (default: 0 for workload 1, else the "
+                         "workload's number)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle baseline's timed work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -270,7 +273,7 @@ def main():
 
     dev = torch.device("cuda:0")
     t0 = time.time()
-    w = W.make_config(args.config)
+    w = W.make_config(args.config, seed=args.seed)
     log("workload %s: %d rows x %d (%s), %.2f GB logits, generated in %.1fs" % (
         w.name, w.rows_per_call, w.vocab, w.dtype, w.logit_bytes_per_call / 1e9, time.time() - t0))
 
@@ -661,6 +664,8 @@ def main():
                                      ", every call with its commit (asd_verify_commit)") +
                                     ", the step captured as one HIP graph and replayed"
                                     if args.graph else "")),
+                   "seed": args.seed if args.seed is not None else (0 if args.config == 1
+                                                                    else args.config),
                    "vocab_shards": args.shards or 1,
                    "calls_per_step": w.blocks,
                    "rows_per_call": w.rows_per_call, "vocab": w.vocab,
@@ -689,7 +694,7 @@ def bench_lmhead(args, torch, asd, W):
     cores, reduced in the epilogue, never written.  Compared with the unfused
     path (a library GEMM writing bf16 logits, then asd_verify)."""
     dev = torch.device("cuda:0")
-    w = W.make_config(args.config)
+    w = W.make_config(args.config, seed=args.seed)
     d = args.lmhead
     rows, V = w.rows_per_call, w.vocab
     g = torch.Generator(device=dev).manual_seed(1234)
