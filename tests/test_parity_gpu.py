@@ -76,6 +76,19 @@ def test_workload_full_size(cfg, variant):
         assert np.array_equal(g["budget"], w.budget)
 
 
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workload_seeds_0_to_9(cfg):
+    """Every workload at seeds 0..9, reduced in batch (full vocabulary), bit-exact."""
+    for seed in range(10):
+        w = W.make_config(cfg, seed=seed, batch={1: 3, 2: 6, 3: 6, 4: 4, 5: 24}[cfg])
+        if w.blocks > 1:
+            lg, dr = w.call(seed % w.blocks)
+            check(lg, dr, w.block_lens, w.tau, w.exc_cap, w.budget, label="%s seed %d" % (
+                w.name, seed))
+        else:
+            check_workload(w, "%s seed %d" % (w.name, seed))
+
+
 def test_workload1_sequential_blocks_carry_the_ledger_on_device():
     """64 sequential calls of one request; the ledger stays in device memory."""
     w = W.make_config(1)
