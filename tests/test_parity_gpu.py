@@ -490,3 +490,49 @@ def test_wavefronts_choose_raw_or_sign_magnitude_keys(dtype, rows, vocab):
     used = int(np.sum(lens + 1))
     check(logits[:used], draft[:used], lens, 1.0, 2, [[4.0, 0.0]] * len(lens),
           label="wave-modes-%s-%dx%d" % (dtype, rows, vocab))
+
+
+# ------------------------------------------------------------- scale limits
+
+def test_very_long_block():
+    """K = 3,000: the scan walks 47 windows of 64 positions."""
+    rng = np.random.default_rng(31)
+    vocab = 512
+    lens = np.array([3000, 5], dtype=np.int32)
+    rows = int(np.sum(lens + 1))
+    z = rng.normal(0, 1, size=(rows, vocab)).astype(np.float32)
+    y = np.argmax(z, axis=1)
+    second = np.argsort(-z, axis=1, kind="stable")[:, 1]
+    draft = np.where(rng.random(rows) < 0.97, y, second).astype(np.int32)
+    check(z, draft, lens, np.inf, 2**31 - 1, [[np.inf, 0.0]] * 2, label="k3000-inf")
+    check(z, draft, lens, 0.01, 40, [[30.0, 0.0]] * 2, label="k3000")
+
+
+def test_seventy_thousand_requests():
+    """A large scan grid and the row kernel's one-workgroup offset scan over
+    70,000 block lengths (K in 0..2, some negative)."""
+    rng = np.random.default_rng(32)
+    n, vocab = 70000, 64
+    lens = rng.integers(-1, 3, n).astype(np.int32)
+    rows = int(np.sum(np.maximum(lens, 0) + 1))
+    table = W.f32_to_bf16(np.arange(-8, 9, dtype=np.float32) / 4)   # dyadic values, many ties
+    logits = table[rng.integers(0, table.size, size=(rows, vocab), dtype=np.int8)]
+    y = oracle.argmax_rows(logits)
+    draft = np.where(rng.random(rows) < 0.6, y, rng.integers(0, vocab, rows)).astype(np.int32)
+    tau = rng.uniform(0, 2, n).astype(np.float32)
+    budget = np.stack([rng.uniform(0, 4, n), np.zeros(n)], 1).astype(np.float32)
+    check(logits, draft, lens, tau, 2, budget, label="70k-requests")
+
+
+def test_vocabulary_of_a_million_splits_at_the_cap():
+    """V = 2^20 over 9 rows: the plan wants more than 64 splits and takes 64."""
+    rng = np.random.default_rng(33)
+    vocab, rows = 1 << 20, 9
+    z = rng.normal(0, 2, size=(rows, vocab)).astype(np.float32)
+    z[3, vocab - 1] = 50.0                       # the maximum in the last split
+    z[5, 0] = 50.0                               # and in the first
+    logits = W.f32_to_bf16(z)
+    y = oracle.argmax_rows(logits)
+    draft = np.where(rng.random(rows) < 0.5, y, rng.integers(0, vocab, rows)).astype(np.int32)
+    check(logits, draft, np.array([8], np.int32), 2.0, 2, [[6.0, 0.0]], label="v2^20")
+    check(z, draft, np.array([8], np.int32), 2.0, 2, [[6.0, 0.0]], label="v2^20-f32")
