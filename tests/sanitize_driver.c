@@ -9,7 +9,8 @@
  * the edge conditions the verifier defines: K = 0 and K < 0, requests whose
  * rows do not fit, explicit offsets with gaps, draft ids outside [0, V),
  * NaN / infinity / signed-zero logits, g in {-1, 0, 0.25, inf, NaN},
- * M in {0, 1, INT32_MAX}, B in {0, -0, tiny, inf} and s = B.
+ * M in {0, 1, INT32_MAX}, B in {0, -0, tiny, inf} and s = B, with and without
+ * the raw-gate flag and the error word.
  */
 #include "../oracle/asd_oracle.c"
 #include "../workloads/gen.c"
@@ -109,9 +110,16 @@ static void run_case(int c)
         regret[r] = 0.0f;
     }
     const int with_rows = (int)pick(2);
-    if (oracle_verify(logits, dtype, vocab, nreq, rows, draft, lens, offs, tau, cap, budget,
-                      acc, nxt, with_rows ? amax : NULL, with_rows ? regret : NULL) != 0) {
-        fprintf(stderr, "case %d: oracle_verify rejected valid arguments\n", c);
+    uint32_t err = 0;
+    const uint32_t flags = pick(3) == 0 ? ORACLE_RAW_GATE : 0u;
+    if (oracle_verify_ex(logits, dtype, vocab, nreq, rows, draft, lens, offs, tau, cap, budget,
+                         acc, nxt, with_rows ? amax : NULL, with_rows ? regret : NULL, flags,
+                         pick(2) ? &err : NULL) != 0) {
+        fprintf(stderr, "case %d: oracle_verify_ex rejected valid arguments\n", c);
+        exit(1);
+    }
+    if (err & ~(ORACLE_ERR_NEGATIVE_K | ORACLE_ERR_ROWS)) {
+        fprintf(stderr, "case %d: unknown error bits %u\n", c, err);
         exit(1);
     }
     for (int32_t i = 0; i < nreq; ++i) {
