@@ -463,3 +463,55 @@ def test_lmhead_logits_exact_regime_equals_integer_matmul():
     z = oracle.lmhead_logits(W.f32_to_bf16(np.zeros((1, 4), np.float32)),
                              W.f32_to_bf16(-np.ones((1, 4), np.float32)))
     assert z[0, 0] == 0.0 and not np.signbit(z[0, 0])
+
+
+# ------------------------------------------------------- metamorphic checks
+
+def _batch(rng, n, vocab):
+    lens = rng.integers(0, 10, n).astype(np.int32)
+    rows = int(np.sum(lens + 1))
+    z = (rng.integers(-8, 9, size=(rows, vocab)) / 4.0).astype(np.float32)
+    y = np.argmax(z, axis=1)
+    draft = np.where(rng.random(rows) < 0.6, y, rng.integers(0, vocab, rows)).astype(np.int32)
+    tau = rng.choice(np.array([0.25, 1.0, 2.0, np.inf], np.float32), n)
+    cap = rng.choice(np.array([0, 1, 3], np.int32), n)
+    budget = np.stack([rng.choice(np.array([0.0, 1.0, 4.0], np.float32), n),
+                       np.zeros(n, np.float32)], 1)
+    return z, draft, lens, tau, cap, budget
+
+
+def test_requests_are_independent_split_and_permuted():
+    """Algorithm 1 runs per request: a batch verified at once equals its two
+    halves verified apart, and a permutation of the requests (their rows moved
+    with them through explicit offsets, with unused rows between) permutes the
+    outputs."""
+    rng = np.random.default_rng(61)
+    for _ in range(60):
+        n, vocab = int(rng.integers(2, 12)), int(rng.integers(1, 20))
+        z, draft, lens, tau, cap, budget = _batch(rng, n, vocab)
+        whole = oracle.verify(z, draft, lens, tau, cap, budget)
+        k = int(rng.integers(1, n))
+        cut = int(np.sum(lens[:k] + 1))
+        a = oracle.verify(z[:cut], draft[:cut], lens[:k], tau[:k], cap[:k], budget[:k])
+        b = oracle.verify(z[cut:], draft[cut:], lens[k:], tau[k:], cap[k:], budget[k:])
+        for key in ("accept_len", "next_token", "budget"):
+            assert np.array_equal(whole[key], np.concatenate([a[key], b[key]]))
+        # permuted requests, rows laid out in the new order with gaps
+        perm = rng.permutation(n)
+        starts = np.concatenate([[0], np.cumsum(lens + 1)])[:-1]
+        blocks, offs, pos = [], [], 0
+        for i in perm:
+            pos += int(rng.integers(0, 3))
+            offs.append(pos)
+            blocks.append((pos, starts[i], lens[i] + 1))
+            pos += lens[i] + 1
+        rows2 = pos + 1
+        z2 = np.full((rows2, vocab), -9.0, np.float32)
+        d2 = np.zeros(rows2, np.int32)
+        for dst, src, cnt in blocks:
+            z2[dst:dst + cnt] = z[src:src + cnt]
+            d2[dst:dst + cnt] = draft[src:src + cnt]
+        p = oracle.verify(z2, d2, lens[perm], tau[perm], cap[perm], budget[perm],
+                          row_offsets=np.array(offs, np.int64))
+        for key in ("accept_len", "next_token", "budget"):
+            assert np.array_equal(p[key], whole[key][perm])

@@ -536,3 +536,42 @@ def test_vocabulary_of_a_million_splits_at_the_cap():
     draft = np.where(rng.random(rows) < 0.5, y, rng.integers(0, vocab, rows)).astype(np.int32)
     check(logits, draft, np.array([8], np.int32), 2.0, 2, [[6.0, 0.0]], label="v2^20")
     check(z, draft, np.array([8], np.int32), 2.0, 2, [[6.0, 0.0]], label="v2^20-f32")
+
+
+# ------------------------------------------------------- metamorphic checks
+
+def test_requests_are_independent_split_and_permuted_on_the_gpu():
+    """A ragged batch verified at once equals its halves verified apart, and a
+    permutation of its requests (rows moved with them, unused rows between)
+    permutes every output; all three agree with the oracle bit for bit."""
+    rng = np.random.default_rng(71)
+    w = W.make_config(5, batch=96, vocab=20000)
+    n = w.num_requests
+    lens = w.block_lens
+    whole = check_workload(w, "independence-whole")
+    k = 37
+    cut = int(np.sum(lens[:k] + 1))
+    a = check(w.logits[:cut], w.draft_tokens[:cut], lens[:k], w.tau[:k], w.exc_cap[:k],
+              w.budget[:k], label="independence-first")
+    b = check(w.logits[cut:], w.draft_tokens[cut:], lens[k:], w.tau[k:], w.exc_cap[k:],
+              w.budget[k:], label="independence-second")
+    for key in ("accept_len", "next_token", "budget"):
+        assert np.array_equal(whole[key], np.concatenate([a[key], b[key]])), key
+    perm = rng.permutation(n)
+    starts = np.concatenate([[0], np.cumsum(lens + 1)])[:-1]
+    offs, pos, moves = [], 0, []
+    for i in perm:
+        pos += int(rng.integers(0, 4))
+        offs.append(pos)
+        moves.append((pos, starts[i], lens[i] + 1))
+        pos += lens[i] + 1
+    rows2 = pos + 3
+    z2 = np.zeros((rows2, w.vocab), np.uint16)
+    d2 = np.zeros(rows2, np.int32)
+    for dst, src, cnt in moves:
+        z2[dst:dst + cnt] = w.logits[src:src + cnt]
+        d2[dst:dst + cnt] = w.draft_tokens[src:src + cnt]
+    p = check(z2, d2, lens[perm], w.tau[perm], w.exc_cap[perm], w.budget[perm],
+              row_offsets=np.array(offs, np.int64), label="independence-permuted")
+    for key in ("accept_len", "next_token", "budget"):
+        assert np.array_equal(p[key], whole[key][perm]), key
