@@ -1209,33 +1209,41 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
     }
 
     // ---- epilogue, through LDS (the stages are free now).  Four passes, one
-    // per 32-row slice i of each wavefront: E0 holds the slice rows of wm = 0,
-    // E1 those of wm = 1, each [32 rows][256 columns] of logit bits, with the
-    // 16-B chunk c of row lr at chunk c ^ ((c >> 4) & 3) ^ 4 (lr & 3) ^
-    // 8 ((lr >> 2) & 1): conflict-free for the stores and for the row scans.
-    // Columns past N are stored as -inf, whose key no value ranks below; a real
-    // column that ties with one wins by its lower index.  Then four
-    // threads scan each of the 64 rows, 64 columns each in increasing order.
+    // per 32-row slice i of each wavefront; pass i uses the stage pair i % 2,
+    // so one barrier per pass separates its stores from its scans.  E0 holds
+    // the slice rows of wm = 0, E1 those of wm = 1, each [32 rows][256
+    // columns] of logit bits, with the 16-B chunk c of row lr at chunk c ^
+    // ((c >> 4) & 3) ^ 4 (lr & 3) ^ 8 ((lr >> 2) & 1): conflict-free for the
+    // stores and for the row scans.  Four threads then scan each of the 64
+    // rows, 64 columns each.
+    //
+    // A scan ranks raw patterns read as signed integers: per 16-B chunk a
+    // signed and an unsigned maximum, and the first chunk with the greatest
+    // signed maximum.  When that maximum is a number in [1, +inf] and the
+    // unsigned maximum shows no NaN with the sign bit set, it is the exact
+    // maximum of the 64 columns and the winning chunk's first element equal
+    // to it is their first maximum.  Otherwise (a NaN, no positive number, or
+    // columns past N, which take no part in the ranking) the thread ranks its
+    // columns again with exact keys.
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no copy outlives the main loop
-    uint32_t* const E0 = (uint32_t*)A0;
-    uint32_t* const E1 = (uint32_t*)B0;
-    uint32_t* const Ew = wm ? E1 : E0;
     int wbase[4];
-    uint32_t wmask[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const int col = wn * 128 + j * 32 + (lane & 31);
         const int cl = col >> 2;
         wbase[j] = 4 * 256 * h + ((cl ^ ((cl >> 4) & 3) ^ (h << 3)) << 2) + (col & 3);
-        wmask[j] = col0 + col < N ? 0u : 0xffffffffu;
     }
     const int rr = tid >> 2, q = tid & 3;                 // scan: slice row, column quarter
     const int lrr = rr & 31;
-    const uint32_t* const Er = (rr < 32 ? E0 : E1) + lrr * 256;
     const int xq = q ^ ((lrr & 3) << 2) ^ (((lrr >> 2) & 1) << 3);
+    const int64_t qcol0 = col0 + q * 64;                  // first column of the quarter
+    const bool qfull = qcol0 + 64 <= N;
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        __syncthreads();
+        uint32_t* const E0 = (uint32_t*)((i & 1) ? A1 : A0);
+        uint32_t* const E1 = (uint32_t*)((i & 1) ? B1 : B0);
+        uint32_t* const Ew = wm ? E1 : E0;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -1244,28 +1252,54 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
                 // cast of the vector element itself read element 0 for every v.
                 const float val = acc[i][j][v];
                 Ew[(wbase[j] ^ ((v & 3) << 4)) + 256 * (8 * (v >> 2) + (v & 3))] =
-                    (__float_as_uint(val) & ~wmask[j]) | (0xff800000u & wmask[j]);
+                    __float_as_uint(val);
             }
         __syncthreads();
         const int r = (rr >> 5) * 128 + i * 32 + lrr;      // tile row
-        int bk = (int)0x80000000, bc = 0;
+        const uint32_t* const Er = (rr < 32 ? E0 : E1) + lrr * 256 + q * 64;
+        unsigned long long best = 0;                       // ranks below every key
+        if (row0 + r < M) {
+            int32_t bm = (int32_t)0x80000000;
+            uint32_t um = 0;
+            int bch = 0;
 #pragma unroll
-        for (int c = 0; c < 16; ++c) {
-            const uint4 f = *(const uint4*)(Er + ((q * 16 + (c ^ xq)) << 2));
-            const uint32_t fv[4] = {f.x, f.y, f.z, f.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int k = f32_key(fv[e]);
-                if (k > bk) {                              // strict: lowest column on ties
-                    bk = k;
-                    bc = c * 4 + e;
+            for (int c = 0; c < 16; ++c) {
+                const uint4 f = *(const uint4*)(Er + ((c ^ xq) << 2));
+                const int32_t m = max(max((int32_t)f.x, (int32_t)f.y), max((int32_t)f.z, (int32_t)f.w));
+                um = max(um, max(max(f.x, f.y), max(f.z, f.w)));
+                if (m > bm) {                              // strict: first chunk on ties
+                    bm = m;
+                    bch = c;
                 }
             }
+            int32_t bk;
+            int bc;
+            if (qfull && bm >= 1 && bm <= KeyTraits<4>::kInf && um <= KeyTraits<4>::kNegInfPattern) {
+                const uint4 f = *(const uint4*)(Er + ((bch ^ xq) << 2));
+                const int e = (int32_t)f.x == bm ? 0 : (int32_t)f.y == bm ? 1 : (int32_t)f.z == bm ? 2 : 3;
+                bk = bm;                                   // a positive number's key is its pattern
+                bc = bch * 4 + e;
+            } else {
+                bk = (int32_t)0x80000000;
+                bc = 0;
+                for (int c = 0; c < 16; ++c) {
+                    const uint4 f = *(const uint4*)(Er + ((c ^ xq) << 2));
+                    const uint32_t fv[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int k = qcol0 + c * 4 + e < N ? f32_key(fv[e]) : (int32_t)0x80000000;
+                        if (k > bk) {                      // strict: lowest column on ties
+                            bk = k;
+                            bc = c * 4 + e;
+                        }
+                    }
+                }
+            }
+            best = pack_kc(bk, qcol0 + bc);
+            const int64_t xo = (int64_t)s_draft[r] - qcol0;
+            if (xo >= 0 && xo < 64 && qcol0 + xo < N)
+                row_draft_bits[row0 + r] = Er[((((int)xo >> 2) ^ xq) << 2) + ((int)xo & 3)];
         }
-        unsigned long long best = pack_kc(bk, col0 + q * 64 + bc);
-        const int64_t xo = (int64_t)s_draft[r] - col0 - q * 64;
-        if (xo >= 0 && xo < 64 && row0 + r < M)
-            row_draft_bits[row0 + r] = Er[((q * 16 + (((int)xo >> 2) ^ xq)) << 2) + ((int)xo & 3)];
         unsigned long long o = __shfl_xor(best, 1, 64);
         best = o > best ? o : best;
         o = __shfl_xor(best, 2, 64);

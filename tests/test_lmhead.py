@@ -84,6 +84,49 @@ def test_exact_regime_bit_exact(rows, vocab, d):
     assert not bad, "differs in %s: %s" % (bad, describe(g, r))
 
 
+@pytest.mark.parametrize("rows,vocab,d", [(130, 1027, 128), (40, 5000, 256), (300, 640, 128)])
+def test_nonfinite_and_negative_rows_bit_exact(rows, vocab, d):
+    """Rows that the epilogue cannot rank by raw patterns: every logit negative,
+    NaNs among infinities, infinities only, NaN everywhere and all-zero rows,
+    mixed with ordinary rows.  Coordinates 0-2 are reserved: weights 1 (a bias
+    that makes a row negative when its hidden value is -256), weights in
+    {-1, 0, 1} (inf there gives NaN where the weight is 0 and +-inf elsewhere),
+    and weights +-0.5 (inf there gives +-inf only)."""
+    from asd_gpu import describe, mismatches
+    rng = np.random.default_rng(rows + vocab + d)
+    h = rng.integers(-2, 3, size=(rows, d)).astype(np.float32)
+    w = (rng.integers(-2, 3, size=(vocab, d)) / 2.0).astype(np.float32)
+    h[:, :3] = 0.0
+    w[:, 0] = 1.0
+    w[:, 1] = rng.integers(-1, 2, size=vocab)
+    w[:, 2] = rng.choice([-0.5, 0.5], size=vocab)
+    kind = rng.integers(0, 7, size=rows)
+    h[kind == 1, 0] = -256.0                      # every logit negative
+    h[kind == 2, 1] = np.inf                      # NaN where w = 0, +-inf elsewhere
+    h[kind == 3, 2] = np.inf                      # +-inf only
+    h[kind == 4, 2] = -np.inf
+    h[kind == 5, 3] = np.nan                      # NaN in every column
+    h[kind == 6] = 0.0                            # every logit zero
+    hidden, weight = W.f32_to_bf16(h), W.f32_to_bf16(w)
+    z = oracle.lmhead_logits(hidden, weight)
+    assert np.isnan(z[kind == 2]).any() and np.isinf(z[kind == 3]).all()
+    assert (z[kind == 1] < 0).all()
+    draft = rng.integers(0, vocab, rows).astype(np.int32)
+    draft[rng.random(rows) < 0.05] = vocab + 1
+    lens = []
+    left = rows
+    while left > 0:
+        k = int(min(left - 1, rng.integers(0, 9)))
+        lens.append(k)
+        left -= k + 1
+    budget = np.stack([rng.uniform(0, 6, len(lens)), np.zeros(len(lens))], axis=1)
+    print("case lmhead nonfinite rows %d vocab %d d %d" % (rows, vocab, d), flush=True)
+    g = _run(hidden, weight, draft, lens, 1.0, 2, budget)
+    r = oracle.lmhead_verify(hidden, weight, draft, lens, 1.0, 2, budget)
+    bad = mismatches(g, r)
+    assert not bad, "differs in %s: %s" % (bad, describe(g, r))
+
+
 def test_realistic_regime_within_rounding_bound():
     rng = np.random.default_rng(12)
     rows, vocab, d = 200, 4000, 1024
