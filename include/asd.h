@@ -114,6 +114,9 @@ typedef struct {
  * streams use different workspaces.  The first call on a (device, stream)
  * pair, or one that needs a larger workspace, allocates device memory
  * (hipMalloc) and so must not happen during stream capture (ASD_ECAPTURE).
+ * A larger workspace is a new buffer of at least twice the size; the buffers
+ * it replaces stay allocated until asd_release, so a graph captured with an
+ * earlier call stays valid after the workspace grows.
  * Returns ASD_OK once the work is enqueued.
  */
 asd_status asd_verify(const void *logits, asd_dtype dtype, int64_t vocab,
@@ -396,8 +399,10 @@ const char *asd_status_string(asd_status status);
 const char *asd_version(void);
 
 /*
- * asd_release -- free every library-owned workspace.  The caller must make
- * sure no enqueued asd_verify call is still running (synchronize first).
+ * asd_release -- free every library-owned workspace, including the buffers
+ * a workspace outgrew.  The caller must make sure no enqueued call that uses
+ * a library workspace is still running (synchronize first), and must not
+ * replay a graph captured with such a call afterwards.
  */
 asd_status asd_release(void);
 

@@ -6,6 +6,7 @@
 #include <map>
 #include <mutex>
 #include <utility>
+#include <vector>
 
 #include "../../include/asd.h"
 #include "asd_plan.h"
@@ -16,9 +17,9 @@ namespace {
 
 size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
 
-// Tiles the row kernel aims for: at least two rounds of the 8 resident
-// 256-thread workgroups per CU, so that the last round's stragglers are a
-// small share of the stream (measured on MI355X: 4,352 whole rows of 297 KB
+// Tiles the row kernel aims for: at least two rounds of the resident 256-thread
+// workgroups per CU (six at the kernel's register budget), so that the last
+// round's stragglers are a small share of the stream (measured on MI355X: 4,352 whole rows of 297 KB
 // stream best unsplit; 2,112 rows of 607 KB gain 5% from two splits).
 constexpr int kTilesPerCu = 16;
 // Smallest split worth its own workgroup, in vectors of 16 bytes.  With at
@@ -69,9 +70,13 @@ Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int32_t num_requests
 
 namespace {
 
+// A library workspace grows by allocating a larger buffer.  The buffers it
+// outgrew stay allocated until asd_release: a graph captured earlier may still
+// hold their addresses, and work already enqueued may still use them.
 struct Workspace {
     void* ptr = nullptr;
     size_t bytes = 0;
+    std::vector<void*> retired;
 };
 
 std::mutex g_mutex;
@@ -170,7 +175,8 @@ asd_status plan_for(asd_dtype dtype, int64_t vocab, int32_t num_requests, int64_
 }
 
 // The library-owned workspace of (current device, stream), grown to at least
-// `bytes`; growth (hipMalloc) is refused during stream capture.
+// `bytes` (and at least doubled, so the retired buffers total less than the
+// current one); growth (hipMalloc) is refused during stream capture.
 asd_status library_workspace(hipStream_t s, size_t bytes, void** out) {
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return ASD_EHIP;
@@ -181,15 +187,11 @@ asd_status library_workspace(hipStream_t s, size_t bytes, void** out) {
         if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ASD_EHIP;
         if (cap != hipStreamCaptureStatusNone) return ASD_ECAPTURE;
         size_t want = bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : bytes;
+        if (want < 2 * w.bytes) want = 2 * w.bytes;
         want = align_up(want, (size_t)1 << 20);
-        if (w.ptr) {
-            if (hipStreamSynchronize(s) != hipSuccess) return ASD_EHIP;
-            (void)hipFree(w.ptr);
-            w.ptr = nullptr;
-            w.bytes = 0;
-        }
         void* p = nullptr;
         if (hipMalloc(&p, want) != hipSuccess) return ASD_ENOMEM;
+        if (w.ptr) w.retired.push_back(w.ptr);
         w.ptr = p;
         w.bytes = want;
     }
@@ -522,6 +524,8 @@ asd_status asd_release(void) {
     asd_status st = ASD_OK;
     for (auto& kv : g_workspaces) {
         if (kv.second.ptr && hipFree(kv.second.ptr) != hipSuccess) st = ASD_EHIP;
+        for (void* old : kv.second.retired)
+            if (hipFree(old) != hipSuccess) st = ASD_EHIP;
     }
     g_workspaces.clear();
     return st;
