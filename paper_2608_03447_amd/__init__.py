@@ -115,6 +115,15 @@ def _per_request(value, n, dtype, device, name):
     return torch.full((n,), value, dtype=dtype, device=device)
 
 
+def _check_vector(t, n, dtype, device, name):
+    """An optional vector argument: None, or a contiguous tensor of this dtype
+    and shape (n,) on `device` (the library reads it through a plain pointer)."""
+    if t is not None and (t.dtype != dtype or t.shape != (n,) or t.device != device
+                          or not t.is_contiguous()):
+        raise ValueError("%s must be a contiguous %s tensor of shape (%d,) on %s"
+                         % (name, dtype, n, device))
+
+
 def _check_logits(logits):
     if logits.dim() != 2 or logits.dtype not in _DTYPES or not logits.is_cuda:
         raise ValueError("logits must be a 2-D float32 or bfloat16 tensor on a GPU")
@@ -135,9 +144,7 @@ def _marshal(dev, rows, draft_tokens, block_lens, tau, exc_cap, budget, row_offs
     if budget.dtype != torch.float32 or budget.shape != (n, 2) or budget.device != dev \
             or not budget.is_contiguous():
         raise ValueError("budget must be a contiguous float32 (%d, 2) tensor on %s" % (n, dev))
-    if row_offsets is not None and (row_offsets.dtype != torch.int64 or row_offsets.shape != (n,)
-                                    or row_offsets.device != dev):
-        raise ValueError("row_offsets must be int64 of shape (%d,) on %s" % (n, dev))
+    _check_vector(row_offsets, n, torch.int64, dev, "row_offsets")
     tau = _per_request(tau, n, torch.float32, dev, "tau")
     exc_cap = _per_request(exc_cap, n, torch.int32, dev, "exc_cap")
     block_lens = block_lens.contiguous()
@@ -356,8 +363,7 @@ def asd_opportunity(draft_tokens, row_argmax, row_regret, vocab, block_lens, tau
             or not counts.is_contiguous() or counts.device != dev:
         raise ValueError("counts must be a contiguous int64 (%d, %d) tensor on %s"
                          % (taus.shape[0], ps.shape[0], dev))
-    if row_offsets is not None and (row_offsets.dtype != torch.int64 or row_offsets.shape != (n,)):
-        raise ValueError("row_offsets must be int64 of shape (%d,)" % n)
+    _check_vector(row_offsets, n, torch.int64, dev, "row_offsets")
     block_lens = block_lens.contiguous()
 
     def p(t):
@@ -393,11 +399,8 @@ def asd_commit(draft_tokens, block_lens, accept_len, next_token, tokens, seq_len
     if tokens.dtype != torch.int32 or tokens.dim() != 2 or tokens.shape[0] != n \
             or not tokens.is_contiguous() or tokens.device != dev:
         raise ValueError("tokens must be a contiguous int32 (%d, capacity) tensor on %s" % (n, dev))
-    if out_committed is not None and (out_committed.dtype != torch.int32
-                                      or out_committed.shape != (n,)):
-        raise ValueError("out_committed must be int32 of shape (%d,)" % n)
-    if row_offsets is not None and (row_offsets.dtype != torch.int64 or row_offsets.shape != (n,)):
-        raise ValueError("row_offsets must be int64 of shape (%d,)" % n)
+    _check_vector(out_committed, n, torch.int32, dev, "out_committed")
+    _check_vector(row_offsets, n, torch.int64, dev, "row_offsets")
 
     def p(t):
         return None if t is None else ctypes.c_void_p(t.data_ptr())
@@ -429,10 +432,7 @@ def asd_verify_commit(logits, draft_tokens, block_lens, tau, exc_cap, budget, to
     if seq_len.dtype != torch.int64 or seq_len.shape != (n,) or not seq_len.is_contiguous() \
             or seq_len.device != dev:
         raise ValueError("seq_len must be a contiguous int64 tensor of shape (%d,) on %s" % (n, dev))
-    if out_committed is not None and (out_committed.dtype != torch.int32
-                                      or out_committed.shape != (n,)
-                                      or out_committed.device != dev):
-        raise ValueError("out_committed must be int32 of shape (%d,) on %s" % (n, dev))
+    _check_vector(out_committed, n, torch.int32, dev, "out_committed")
     if workspace is not None and (workspace.dtype != torch.uint8 or not workspace.is_contiguous()
                                   or workspace.device != dev):
         raise ValueError("workspace must be a contiguous uint8 tensor on %s" % dev)

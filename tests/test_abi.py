@@ -320,3 +320,40 @@ def test_read_probe_rejects_invalid_arguments(args):
     vp = lambda v: None if v is None else ctypes.c_void_p(v)
     buf, rows, row_bytes, out = args
     assert lib.asd_read_probe(vp(buf), rows, row_bytes, vp(out), None) == 1
+
+
+def test_binding_rejects_strided_or_misplaced_vectors():
+    """The binding passes plain pointers, so an optional vector must be a dense
+    tensor of the right dtype and shape on the call's device; a strided view
+    is refused before any call (host tensors here, so nothing reaches a GPU)."""
+    import torch
+    cpu = torch.device("cpu")
+    n = 4
+    draft = torch.zeros(3 * n, dtype=torch.int32)
+    lens = torch.full((n,), 2, dtype=torch.int32)
+    budget = torch.zeros(n, 2)
+    strided64 = torch.zeros(2 * n, dtype=torch.int64)[::2]
+    strided32 = torch.zeros(2 * n, dtype=torch.int32)[::2]
+    assert strided64.shape == (n,) and not strided64.is_contiguous()
+    with pytest.raises(ValueError, match="row_offsets"):
+        asd._marshal(cpu, 3 * n, draft, lens, 1.0, 1, budget, strided64, None, None, None, None)
+    with pytest.raises(ValueError, match="row_offsets"):
+        asd._marshal(cpu, 3 * n, draft, lens, 1.0, 1, budget,
+                     torch.zeros(n, dtype=torch.int32), None, None, None, None)
+    acc = torch.zeros(n, dtype=torch.int32)
+    nxt = torch.zeros(n, dtype=torch.int32)
+    tokens = torch.zeros(n, 8, dtype=torch.int32)
+    seq = torch.zeros(n, dtype=torch.int64)
+    with pytest.raises(ValueError, match="row_offsets"):
+        asd.asd_commit(draft, lens, acc, nxt, tokens, seq, row_offsets=strided64)
+    with pytest.raises(ValueError, match="out_committed"):
+        asd.asd_commit(draft, lens, acc, nxt, tokens, seq, out_committed=strided32)
+    amax = torch.zeros(3 * n, dtype=torch.int32)
+    regret = torch.zeros(3 * n)
+    taus = torch.zeros(2)
+    ps = torch.ones(2, dtype=torch.int32)
+    counts = torch.zeros(2, 2, dtype=torch.int64)
+    mism = torch.zeros(1, dtype=torch.int64)
+    with pytest.raises(ValueError, match="row_offsets"):
+        asd.asd_opportunity(draft, amax, regret, 100, lens, taus, ps, counts, mism,
+                            row_offsets=strided64)
