@@ -127,6 +127,53 @@ def test_nonfinite_and_negative_rows_bit_exact(rows, vocab, d):
     assert not bad, "differs in %s: %s" % (bad, describe(g, r))
 
 
+def _fuzz_case(seed):
+    """One random exact-regime case: shape, row kinds (as in the non-finite
+    test), drafts and batch layout all drawn from the seed."""
+    rng = np.random.default_rng(1000 + seed)
+    rows = int(rng.integers(1, 700))
+    vocab = int(rng.integers(1, 3000))
+    d = int(rng.choice([128, 256, 384, 512]))
+    h = rng.integers(-2, 3, size=(rows, d)).astype(np.float32)
+    w = (rng.integers(-2, 3, size=(vocab, d)) / 2.0).astype(np.float32)
+    h[:, :3] = 0.0
+    w[:, 0] = 1.0
+    w[:, 1] = rng.integers(-1, 2, size=vocab)
+    w[:, 2] = rng.choice([-0.5, 0.5], size=vocab)
+    p_special = rng.choice([0.0, 0.05, 0.3])
+    kind = np.where(rng.random(rows) < p_special, rng.integers(1, 7, size=rows), 0)
+    h[kind == 1, 0] = -256.0
+    h[kind == 2, 1] = np.inf
+    h[kind == 3, 2] = np.inf
+    h[kind == 4, 2] = -np.inf
+    h[kind == 5, 3] = np.nan
+    h[kind == 6] = 0.0
+    draft = rng.integers(0, vocab, rows).astype(np.int32)
+    draft[rng.random(rows) < 0.05] = -1
+    lens = []
+    left = rows
+    while left > 0:
+        k = int(min(left - 1, rng.integers(0, 12)))
+        lens.append(k)
+        left -= k + 1
+    budget = np.stack([rng.uniform(0, 6, len(lens)), np.zeros(len(lens))], axis=1)
+    return rows, vocab, d, W.f32_to_bf16(h), W.f32_to_bf16(w), draft, lens, budget
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_fuzz_exact_regime_bit_exact(seed):
+    """Random shapes (ragged row and column tiles, partly valid column quarters,
+    one to four K steps) with ordinary and special rows mixed: every output
+    bit-exact against the oracle."""
+    from asd_gpu import describe, mismatches
+    rows, vocab, d, hidden, weight, draft, lens, budget = _fuzz_case(seed)
+    print("case lmhead fuzz seed %d rows %d vocab %d d %d" % (seed, rows, vocab, d), flush=True)
+    g = _run(hidden, weight, draft, lens, 1.0, 2, budget)
+    r = oracle.lmhead_verify(hidden, weight, draft, lens, 1.0, 2, budget)
+    bad = mismatches(g, r)
+    assert not bad, "seed %d differs in %s: %s" % (seed, bad, describe(g, r))
+
+
 def test_realistic_regime_within_rounding_bound():
     rng = np.random.default_rng(12)
     rows, vocab, d = 200, 4000, 1024
