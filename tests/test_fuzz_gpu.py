@@ -1,7 +1,7 @@
-"""Randomized parity sweep: many small verifier calls with random shapes,
-layouts, controls and special values, each compared bit for bit with the
-oracle (accept lengths, next tokens, per-row argmax and regret, the ledger,
-the commit and the device error word)."""
+"""Randomized parity sweep: many verifier calls with random shapes (whole rows
+and split plans), layouts, controls and special values, each compared bit for
+bit with the oracle (accept lengths, next tokens, per-row argmax and regret,
+the ledger, the commit and the device error word)."""
 import numpy as np
 import pytest
 import torch
@@ -19,10 +19,17 @@ SPECIAL_F32 = np.array([0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC000
                        dtype=np.uint32)
 
 
-def _case(rng):
+def _case(rng, large_vocab=False):
+    """One random call.  With `large_vocab` the vocabulary is 8,191 to 151,936
+    entries and there are at most six requests, so rows are split over several
+    workgroups (a split plan); otherwise V <= 5,003 and rows are whole."""
     dtype = "bf16" if rng.random() < 0.6 else "f32"
-    vocab = int(rng.choice([1, 2, 7, 64, 257, 1000, 1031, 4096, 5003]))
-    n = int(rng.integers(1, 40))
+    if large_vocab:
+        vocab = int(rng.choice([8191, 16385, 32000, 50257, 129280, 151936]))
+        n = int(rng.integers(1, 7))
+    else:
+        vocab = int(rng.choice([1, 2, 7, 64, 257, 1000, 1031, 4096, 5003]))
+        n = int(rng.integers(1, 40))
     lens = rng.integers(-2, 20, n).astype(np.int32)
     offsets = None
     rows = int(np.sum(np.maximum(lens, 0) + 1))
@@ -64,13 +71,21 @@ def _case(rng):
 
 @pytest.mark.parametrize("block", range(6))
 def test_random_calls_match_the_oracle(block):
-    rng = np.random.default_rng(5000 + block)
+    _run_block(np.random.default_rng(5000 + block), "fuzz %d" % block, large_vocab=False)
+
+
+@pytest.mark.parametrize("block", range(2))
+def test_random_split_plan_calls_match_the_oracle(block):
+    _run_block(np.random.default_rng(7000 + block), "fuzz-split %d" % block, large_vocab=True)
+
+
+def _run_block(rng, name, large_vocab):
     for case in range(25):
-        dtype, logits, draft, lens, offsets, tau, cap, budget, raw_gate = _case(rng)
+        dtype, logits, draft, lens, offsets, tau, cap, budget, raw_gate = _case(rng, large_vocab)
         rows, vocab = logits.shape
         n = len(lens)
-        label = "fuzz %d.%d: %s rows %d vocab %d requests %d offsets %s raw_gate %s" % (
-            block, case, dtype, rows, vocab, n, offsets is not None, raw_gate)
+        label = "%s.%d: %s rows %d vocab %d requests %d offsets %s raw_gate %s" % (
+            name, case, dtype, rows, vocab, n, offsets is not None, raw_gate)
         print(label, flush=True)
         ref = oracle.verify(logits, draft, lens, tau, cap, budget, offsets, raw_gate=raw_gate)
         capacity = 24
