@@ -1034,11 +1034,13 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
 // each row's greatest (key, column) and the draft token's logit: the M x N
 // logits never reach memory.
 //
-// One workgroup per 256 x 256 output tile; four wavefronts in 2 x 2, each
-// 128 x 128 as 4 x 4 MFMA tiles whose accumulators live in AGPRs.  MFMA
-// operand layout (lane l, element e): A row l % 32, k = 8 (l / 32) + e; B
-// column l % 32, same k; accumulator v of lane l is row 8 (v / 4) + 4 (l / 32)
-// + v % 4, column l % 32.
+// One workgroup of eight wavefronts per 256 x 256 output tile, two per SIMD:
+// wavefront w covers rows 128 (w / 4) .. + 128 and columns 64 (w % 4) .. + 64
+// as 4 x 2 MFMA tiles whose 128 accumulators per lane live in AGPRs.  With
+// two wavefronts per SIMD one issues while the other waits on its LDS reads or
+// at the barrier.  MFMA operand layout (lane l, element e): A row l % 32,
+// k = 8 (l / 32) + e; B column l % 32, same k; accumulator v of lane l is row
+// 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32.
 //
 // K steps of 64 go through two LDS stages per operand, each [256 rows][128 B].
 // Global -> LDS copies are buffer loads that write LDS directly (no VGPR
@@ -1049,11 +1051,12 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
 // alias the fragment reads from the other.
 //
 // Software pipeline of one wavefront: the fragments of the next k-slice are
-// read while the current slice's 16 MFMAs issue (one LDS read per MFMA), and
+// read while the current slice's 8 MFMAs issue (one LDS read per MFMA), and
 // the barrier that publishes the next stage sits before the last slice's
 // MFMAs, so the next stage's first reads and copies overlap them.
 constexpr int kLmTile = 256;
 constexpr int kLmK = 64;
+constexpr int kLmThreads = 512;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -1065,11 +1068,15 @@ constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data format
 __device__ __forceinline__ int lm_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // One stage of one operand: tile rows 0..255, columns [k0b / 2, k0b / 2 + 64).
-// Row r of the tile starts at byte r * K2 of the buffer.  Wavefront w copies
-// the 1-KB blocks w, w + 4, ..., each 8 rows; lane l fills 16-B position l % 8
-// of row l / 8 with k-chunk (l % 8) ^ lm_swz(row).
+// Row r of the tile starts at byte r * K2 of the buffer.  Wavefronts 0..3, one
+// per SIMD, copy; wavefront w copies the 1-KB blocks w, w + 4, ..., w + 28,
+// each 8 rows, and lane l fills 16-B position l % 8 of row l / 8 with k-chunk
+// (l % 8) ^ lm_swz(row).  The other wavefront of each SIMD issues none, so it
+// keeps the matrix core busy while its partner's copies are issued (measured
+// faster than all eight wavefronts copying four blocks each).
 __device__ __forceinline__ void lm_copy_stage(rsrc_t rs, int K2, int k0b, int wave, int lane,
                                               __bf16* lds) {
+    if (wave >= 4) return;
     const int c = (lane & 7) ^ (lane >> 3) ^ (wave & 1);   // (lane & 7) ^ lm_swz(row)
     const int voff = (wave * 8 + (lane >> 3)) * K2 + c * 16;
 #pragma unroll
@@ -1081,40 +1088,42 @@ __device__ __forceinline__ void lm_copy_stage(rsrc_t rs, int K2, int k0b, int wa
 }
 
 __device__ __forceinline__ void lm_frags(const __bf16* Ar, const __bf16* Br, int p,
-                                         bf16x8 (&a)[4], bf16x8 (&b)[4]) {
+                                         bf16x8 (&a)[4], bf16x8 (&b)[2]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(Ar + i * 32 * kLmK + p);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Br + j * 32 * kLmK + p);
+    for (int j = 0; j < 2; ++j) b[j] = *(const bf16x8*)(Br + j * 32 * kLmK + p);
 }
 
-__device__ __forceinline__ void lm_mfma16(const bf16x8 (&a)[4], const bf16x8 (&b)[4],
-                                          f32x16 (&acc)[4][4]) {
+__device__ __forceinline__ void lm_mfma8(const bf16x8 (&a)[4], const bf16x8 (&b)[2],
+                                         f32x16 (&acc)[4][2]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
 }
 
-// Interleave: one MFMA, then one LDS read, eight times, then eight MFMAs; the
-// variant for the stage boundary also spreads the 16 buffer copies.
+// Interleave: one MFMA, then one LDS read, six times, then two MFMAs; the
+// variant for the stage boundary also spreads a copying wavefront's buffer
+// copies.
 #define LM_SCHED_READS()                                                     \
     do {                                                                     \
-        _Pragma("unroll") for (int t_ = 0; t_ < 8; ++t_) {                   \
+        _Pragma("unroll") for (int t_ = 0; t_ < 6; ++t_) {                   \
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);               \
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);               \
         }                                                                    \
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                   \
     } while (0)
 #define LM_SCHED_READS_COPIES()                                              \
     do {                                                                     \
-        _Pragma("unroll") for (int t_ = 0; t_ < 8; ++t_) {                   \
+        _Pragma("unroll") for (int t_ = 0; t_ < 6; ++t_) {                   \
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);               \
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);               \
-            __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);               \
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);               \
         }                                                                    \
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                   \
+        __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);                   \
     } while (0)
 
 struct LmCtx {
@@ -1128,13 +1137,13 @@ struct LmCtx {
 // it (k0b) and the next stage's first fragments are read.
 __device__ __forceinline__ void lm_step(const LmCtx& x, const __bf16* Ac, const __bf16* Bc,
                                         const __bf16* An, const __bf16* Bn, int k0b,
-                                        bf16x8 (&fa)[2][4], bf16x8 (&fb)[2][4],
-                                        f32x16 (&acc)[4][4]) {
+                                        bf16x8 (&fa)[2][4], bf16x8 (&fb)[2][2],
+                                        f32x16 (&acc)[4][2]) {
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
         lm_frags(Ac + x.offA, Bc + x.offB, ((2 * (kk + 1) + x.h) ^ x.sw) * 8, fa[(kk + 1) & 1],
                  fb[(kk + 1) & 1]);
-        lm_mfma16(fa[kk & 1], fb[kk & 1], acc);
+        lm_mfma8(fa[kk & 1], fb[kk & 1], acc);
         LM_SCHED_READS();
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this lane's copies of (An, Bn)
@@ -1142,11 +1151,11 @@ __device__ __forceinline__ void lm_step(const LmCtx& x, const __bf16* Ac, const 
     lm_copy_stage(x.rh, x.K2, k0b, x.wave, x.lane, (__bf16*)Ac);
     lm_copy_stage(x.rw, x.K2, k0b, x.wave, x.lane, (__bf16*)Bc);
     lm_frags(An + x.offA, Bn + x.offB, (x.h ^ x.sw) * 8, fa[0], fb[0]);
-    lm_mfma16(fa[1], fb[1], acc);
+    lm_mfma8(fa[1], fb[1], acc);
     LM_SCHED_READS_COPIES();
 }
 
-__global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
+__global__ __launch_bounds__(kLmThreads) void asd_lmhead_kernel(
     const unsigned char* __restrict__ hidden, const unsigned char* __restrict__ weight,
     int64_t M, int64_t N, int64_t K, int64_t tiles_m, int64_t tiles,
     const int32_t* __restrict__ draft_tokens, unsigned long long* __restrict__ row_best,
@@ -1157,24 +1166,30 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
     __shared__ __attribute__((aligned(1024))) __bf16 B1[kLmTile * kLmK];
     __shared__ int32_t s_draft[kLmTile];
 
-    // XCD-aware order: workgroup i runs on XCD i % 8; each XCD takes a run of
-    // consecutive tiles, row tiles fastest, so one weight tile is read from
-    // HBM once and serves every row tile from that XCD's L2.
+    // XCD-aware order: workgroup i runs on XCD i % 8, and each XCD takes a run
+    // of consecutive positions.  Positions run over pairs of weight tiles
+    // (slowest), row tiles, then the two weight tiles of the pair (fastest):
+    // the two tiles of a pair start together and read each hidden-state slice
+    // once between them from L2, and a pair of weight tiles is read from HBM
+    // once for all the row tiles that the XCD runs alongside.
     const int64_t per_xcd = gridDim.x / 8;
     const int64_t linear = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    if (linear >= tiles) return;
-    const int64_t row0 = (linear % tiles_m) * kLmTile, col0 = (linear / tiles_m) * kLmTile;
+    const int64_t tiles_n = (N + kLmTile - 1) / kLmTile;
+    const int64_t pair = linear / (2 * tiles_m), within = linear % (2 * tiles_m);
+    const int64_t rt = within >> 1, ct = pair * 2 + (within & 1);
+    if (linear >= tiles || ct >= tiles_n) return;
+    const int64_t row0 = rt * kLmTile, col0 = ct * kLmTile;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar LDS targets
-    const int wm = wave >> 1, wn = wave & 1, h = lane >> 5;
-    s_draft[tid] = row0 + tid < M ? draft_tokens[row0 + tid] : -1;
+    const int wm = wave >> 2, wn = wave & 3, h = lane >> 5;
+    if (tid < kLmTile) s_draft[tid] = row0 + tid < M ? draft_tokens[row0 + tid] : -1;
 
-    f32x16 acc[4][4];
+    f32x16 acc[4][2];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16)(0.0f);
+        for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16)(0.0f);
 
     LmCtx x;
     x.K2 = (int)(K * 2);
@@ -1189,13 +1204,13 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
     x.h = h;
     x.sw = lm_swz(lane & 31);
     x.offA = (wm * 128 + (lane & 31)) * kLmK;
-    x.offB = (wn * 128 + (lane & 31)) * kLmK;
+    x.offB = (wn * 64 + (lane & 31)) * kLmK;
 
     // K / 64 is even.  Copies past the last stage are clamped to it: they
     // refill a stage that is no longer read, and the fragments read after the
     // last stage are never used.
     const int64_t KT = K / kLmK;
-    bf16x8 fa[2][4], fb[2][4];
+    bf16x8 fa[2][4], fb[2][2];
     lm_copy_stage(x.rh, x.K2, 0, wave, lane, A0);
     lm_copy_stage(x.rw, x.K2, 0, wave, lane, B0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -1213,31 +1228,31 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
     // so one barrier per pass separates its stores from its scans.  E0 holds
     // the slice rows of wm = 0, E1 those of wm = 1, each [32 rows][256
     // columns] of logit bits, with the 16-B chunk c of row lr at chunk c ^
-    // ((c >> 4) & 3) ^ 4 (lr & 3) ^ 8 ((lr >> 2) & 1): conflict-free for the
-    // stores and for the row scans.  Four threads then scan each of the 64
-    // rows, 64 columns each.
+    // ((c >> 4) & 3) ^ 4 (lr & 3) ^ 8 ((lr >> 2) & 1), which keeps the stores
+    // free of bank conflicts.  Eight threads then scan each of the 64 rows, 32
+    // columns each.
     //
     // A scan ranks raw patterns read as signed integers: per 16-B chunk a
     // signed and an unsigned maximum, and the first chunk with the greatest
     // signed maximum.  When that maximum is a number in [1, +inf] and the
     // unsigned maximum shows no NaN with the sign bit set, it is the exact
-    // maximum of the 64 columns and the winning chunk's first element equal
+    // maximum of the 32 columns and the winning chunk's first element equal
     // to it is their first maximum.  Otherwise (a NaN, no positive number, or
     // columns past N, which take no part in the ranking) the thread ranks its
     // columns again with exact keys.
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no copy outlives the main loop
-    int wbase[4];
+    int wbase[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int col = wn * 128 + j * 32 + (lane & 31);
+    for (int j = 0; j < 2; ++j) {
+        const int col = wn * 64 + j * 32 + (lane & 31);
         const int cl = col >> 2;
         wbase[j] = 4 * 256 * h + ((cl ^ ((cl >> 4) & 3) ^ (h << 3)) << 2) + (col & 3);
     }
-    const int rr = tid >> 2, q = tid & 3;                 // scan: slice row, column quarter
+    const int rr = tid >> 3, q = tid & 7;                 // scan: slice row, column eighth
     const int lrr = rr & 31;
-    const int xq = q ^ ((lrr & 3) << 2) ^ (((lrr >> 2) & 1) << 3);
-    const int64_t qcol0 = col0 + q * 64;                  // first column of the quarter
-    const bool qfull = qcol0 + 64 <= N;
+    const int xr = ((lrr & 3) << 2) ^ (((lrr >> 2) & 1) << 3);
+    const int64_t qcol0 = col0 + q * 32;                  // first column of the eighth
+    const bool qfull = qcol0 + 32 <= N;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -1245,7 +1260,7 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
         uint32_t* const E1 = (uint32_t*)((i & 1) ? B1 : B0);
         uint32_t* const Ew = wm ? E1 : E0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 // The element is copied out before its bits are taken: a bit
@@ -1256,15 +1271,19 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
             }
         __syncthreads();
         const int r = (rr >> 5) * 128 + i * 32 + lrr;      // tile row
-        const uint32_t* const Er = (rr < 32 ? E0 : E1) + lrr * 256 + q * 64;
+        const uint32_t* const Er = (rr < 32 ? E0 : E1) + lrr * 256;
+        auto chunk = [&](int c) {                          // chunk c of this thread's eighth
+            const int cl = q * 8 + c;
+            return *(const uint4*)(Er + ((cl ^ ((cl >> 4) & 3) ^ xr) << 2));
+        };
         unsigned long long best = 0;                       // ranks below every key
         if (row0 + r < M) {
             int32_t bm = (int32_t)0x80000000;
             uint32_t um = 0;
             int bch = 0;
 #pragma unroll
-            for (int c = 0; c < 16; ++c) {
-                const uint4 f = *(const uint4*)(Er + ((c ^ xq) << 2));
+            for (int c = 0; c < 8; ++c) {
+                const uint4 f = chunk(c);
                 const int32_t m = max(max((int32_t)f.x, (int32_t)f.y), max((int32_t)f.z, (int32_t)f.w));
                 um = max(um, max(max(f.x, f.y), max(f.z, f.w)));
                 if (m > bm) {                              // strict: first chunk on ties
@@ -1275,15 +1294,15 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
             int32_t bk;
             int bc;
             if (qfull && bm >= 1 && bm <= KeyTraits<4>::kInf && um <= KeyTraits<4>::kNegInfPattern) {
-                const uint4 f = *(const uint4*)(Er + ((bch ^ xq) << 2));
+                const uint4 f = chunk(bch);
                 const int e = (int32_t)f.x == bm ? 0 : (int32_t)f.y == bm ? 1 : (int32_t)f.z == bm ? 2 : 3;
                 bk = bm;                                   // a positive number's key is its pattern
                 bc = bch * 4 + e;
             } else {
                 bk = (int32_t)0x80000000;
                 bc = 0;
-                for (int c = 0; c < 16; ++c) {
-                    const uint4 f = *(const uint4*)(Er + ((c ^ xq) << 2));
+                for (int c = 0; c < 8; ++c) {
+                    const uint4 f = chunk(c);
                     const uint32_t fv[4] = {f.x, f.y, f.z, f.w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -1297,12 +1316,17 @@ __global__ __launch_bounds__(kRowThreads) void asd_lmhead_kernel(
             }
             best = pack_kc(bk, qcol0 + bc);
             const int64_t xo = (int64_t)s_draft[r] - qcol0;
-            if (xo >= 0 && xo < 64 && qcol0 + xo < N)
-                row_draft_bits[row0 + r] = Er[((((int)xo >> 2) ^ xq) << 2) + ((int)xo & 3)];
+            if (xo >= 0 && xo < 32 && qcol0 + xo < N) {
+                const uint4 f = chunk((int)xo >> 2);
+                const uint32_t fv[4] = {f.x, f.y, f.z, f.w};
+                row_draft_bits[row0 + r] = fv[(int)xo & 3];
+            }
         }
         unsigned long long o = __shfl_xor(best, 1, 64);
         best = o > best ? o : best;
         o = __shfl_xor(best, 2, 64);
+        best = o > best ? o : best;
+        o = __shfl_xor(best, 4, 64);
         best = o > best ? o : best;
         if (q == 0 && row0 + r < M) atomicMax(row_best + row0 + r, best);
     }
@@ -1442,9 +1466,10 @@ hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t 
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     const int64_t tiles_m = (rows + kLmTile - 1) / kLmTile;
-    const int64_t tiles = tiles_m * ((vocab + kLmTile - 1) / kLmTile);
+    // positions: row tiles x the weight tiles rounded up to whole pairs
+    const int64_t tiles = tiles_m * 2 * (((vocab + kLmTile - 1) / kLmTile + 1) / 2);
     const int64_t grid = (tiles + 7) / 8 * 8;
-    asd_lmhead_kernel<<<(unsigned)grid, kRowThreads, 0, stream>>>(
+    asd_lmhead_kernel<<<(unsigned)grid, kLmThreads, 0, stream>>>(
         (const unsigned char*)hidden, (const unsigned char*)weight, rows, vocab, d, tiles_m,
         tiles, a.draft_tokens, best, draft_bits);
     if ((err = hipGetLastError()) != hipSuccess) return err;
