@@ -469,8 +469,9 @@ asd_status asd_lmhead_verify(const void* hidden, const void* weight, int64_t d, 
     if (st != ASD_OK || num_requests == 0) return st;
     if (!weight || d < 128 || d % 128 != 0 || d > ((int64_t)1 << 20)) return ASD_EINVAL;
     if (((uintptr_t)hidden & 15) != 0 || ((uintptr_t)weight & 15) != 0) return ASD_EINVAL;
-    // grid positions: row tiles x weight tiles rounded up to whole pairs
-    const int64_t tiles = ((total_rows + 255) / 256) * 2 * (((vocab + 255) / 256 + 1) / 2);
+    // grid positions: row tiles x weight tiles rounded up to whole groups
+    const int64_t tiles = ((total_rows + 255) / 256) * kLmheadGroup *
+                          (((vocab + 255) / 256 + kLmheadGroup - 1) / kLmheadGroup);
     if (tiles >= ((int64_t)1 << 31) - 8) return ASD_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;

@@ -1057,6 +1057,7 @@ __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
 constexpr int kLmTile = 256;
 constexpr int kLmK = 64;
 constexpr int kLmThreads = 512;
+constexpr int kLmGroup = kLmheadGroup;   // weight tiles that share a hidden-state row tile
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -1167,16 +1168,16 @@ __global__ __launch_bounds__(kLmThreads) void asd_lmhead_kernel(
     __shared__ int32_t s_draft[kLmTile];
 
     // XCD-aware order: workgroup i runs on XCD i % 8, and each XCD takes a run
-    // of consecutive positions.  Positions run over pairs of weight tiles
-    // (slowest), row tiles, then the two weight tiles of the pair (fastest):
-    // the two tiles of a pair start together and read each hidden-state slice
-    // once between them from L2, and a pair of weight tiles is read from HBM
-    // once for all the row tiles that the XCD runs alongside.
+    // of consecutive positions.  Positions run over groups of kLmGroup weight
+    // tiles (slowest), row tiles, then the weight tiles of the group (fastest):
+    // the tiles of a group start together and read each hidden-state slice
+    // once between them from L2, and a group of weight tiles serves the row
+    // tiles that the XCD runs alongside it.
     const int64_t per_xcd = gridDim.x / 8;
     const int64_t linear = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
     const int64_t tiles_n = (N + kLmTile - 1) / kLmTile;
-    const int64_t pair = linear / (2 * tiles_m), within = linear % (2 * tiles_m);
-    const int64_t rt = within >> 1, ct = pair * 2 + (within & 1);
+    const int64_t group = linear / (kLmGroup * tiles_m), within = linear % (kLmGroup * tiles_m);
+    const int64_t rt = within / kLmGroup, ct = group * kLmGroup + within % kLmGroup;
     if (linear >= tiles || ct >= tiles_n) return;
     const int64_t row0 = rt * kLmTile, col0 = ct * kLmTile;
 
@@ -1466,8 +1467,9 @@ hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t 
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     const int64_t tiles_m = (rows + kLmTile - 1) / kLmTile;
-    // positions: row tiles x the weight tiles rounded up to whole pairs
-    const int64_t tiles = tiles_m * 2 * (((vocab + kLmTile - 1) / kLmTile + 1) / 2);
+    // positions: row tiles x the weight tiles rounded up to whole groups
+    const int64_t tiles =
+        tiles_m * kLmGroup * (((vocab + kLmTile - 1) / kLmTile + kLmGroup - 1) / kLmGroup);
     const int64_t grid = (tiles + 7) / 8 * 8;
     asd_lmhead_kernel<<<(unsigned)grid, kLmThreads, 0, stream>>>(
         (const unsigned char*)hidden, (const unsigned char*)weight, rows, vocab, d, tiles_m,

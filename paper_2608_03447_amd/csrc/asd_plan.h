@@ -134,6 +134,9 @@ inline size_t lmhead_offsets_offset(int64_t rows) {
 inline size_t lmhead_workspace_bytes(int64_t rows, int32_t num_requests) {
     return lmhead_offsets_offset(rows) + ((size_t)num_requests * 8 + 255) / 256 * 256;
 }
+// LM-head tiles are 256 x 256; grid positions run over whole groups of
+// kLmheadGroup weight tiles (the kernel's tile order).
+constexpr int kLmheadGroup = 4;
 hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t d,
                                 int64_t vocab, int64_t rows, const CallArgs& a, void* workspace,
                                 hipStream_t stream);
