@@ -127,6 +127,23 @@ def test_nonfinite_and_negative_rows_bit_exact(rows, vocab, d):
     assert not bad, "differs in %s: %s" % (bad, describe(g, r))
 
 
+def test_maximum_hidden_size_bit_exact():
+    """d = 2^20, the largest hidden size the call accepts: the copies reach
+    their largest offsets (255 rows of 2 MB) and the K loop runs 16,384
+    steps.  Exact regime: every partial sum is a multiple of 1/2 below 2^22."""
+    from asd_gpu import describe, mismatches
+    rng = np.random.default_rng(20)
+    rows, vocab, d = 4, 257, 1 << 20
+    hidden = W.f32_to_bf16(rng.integers(-2, 3, size=(rows, d)).astype(np.float32))
+    weight = W.f32_to_bf16((rng.integers(-2, 3, size=(vocab, d)) / 2.0).astype(np.float32))
+    draft = rng.integers(0, vocab, rows).astype(np.int32)
+    print("case lmhead rows %d vocab %d d %d" % (rows, vocab, d), flush=True)
+    g = _run(hidden, weight, draft, [3], 1.0, 2, [[4.0, 0.0]])
+    r = oracle.lmhead_verify(hidden, weight, draft, [3], 1.0, 2, [[4.0, 0.0]])
+    bad = mismatches(g, r)
+    assert not bad, "differs in %s: %s" % (bad, describe(g, r))
+
+
 def _fuzz_case(seed):
     """One random exact-regime case: shape, row kinds (as in the non-finite
     test), drafts and batch layout all drawn from the seed."""
