@@ -127,6 +127,50 @@ def test_nonfinite_and_negative_rows_bit_exact(rows, vocab, d):
     assert not bad, "differs in %s: %s" % (bad, describe(g, r))
 
 
+def test_full_size_sampled_rows_bit_exact():
+    """The headline batch at full size in the launch configuration the bench
+    times: 4,352 rows x d 5,120 x V 151,936, exact-regime inputs made on the
+    device.  For sampled draft rows, the oracle forms the exact logits (the
+    weights copied back in chunks) and verifies each as a one-position block;
+    the row's argmax and regret must match bit for bit."""
+    import torch
+    import paper_2608_03447_amd as asd
+    dev = torch.device("cuda:0")
+    w = W.make_config(3)
+    rows, vocab, d = w.rows_per_call, w.vocab, 5120
+    g = torch.Generator(device=dev).manual_seed(77)
+    hidden = torch.randint(-2, 3, (rows, d), generator=g, device=dev).to(torch.bfloat16)
+    weight = (torch.randint(-2, 3, (vocab, d), generator=g, device=dev).to(torch.float32) / 2.0
+              ).to(torch.bfloat16)
+    draft = torch.from_numpy(w.draft_tokens).to(dev)
+    amax = torch.full((rows,), -7, dtype=torch.int32, device=dev)
+    regret = torch.full((rows,), float("nan"), dtype=torch.float32, device=dev)
+    print("case lmhead full size %d x %d x %d" % (rows, d, vocab), flush=True)
+    asd.asd_lmhead_verify(hidden, weight, draft, torch.from_numpy(w.block_lens).to(dev),
+                          torch.from_numpy(w.tau).to(dev), torch.from_numpy(w.exc_cap).to(dev),
+                          torch.from_numpy(w.budget.copy()).to(dev), out_argmax=amax,
+                          out_regret=regret)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    k = w.block_lens[0]
+    sample = np.sort(rng.choice(rows // (k + 1), 12, replace=False)) * (k + 1) + rng.integers(0, k, 12)
+    h_bits = hidden[torch.from_numpy(sample).to(dev)].view(torch.int16).cpu().numpy().view(np.uint16)
+    z = np.concatenate([oracle.lmhead_logits(
+        h_bits, weight[c:c + 16384].view(torch.int16).cpu().numpy().view(np.uint16))
+        for c in range(0, vocab, 16384)], axis=1)
+    # each sampled row as its draft row of a one-position block (its copy as the bonus row)
+    pairs = np.repeat(z, 2, axis=0)
+    dr = np.repeat(w.draft_tokens[sample], 2).astype(np.int32)
+    n = len(sample)
+    r = oracle.verify(pairs, dr, np.ones(n, np.int32), 1.0, 1,
+                      np.zeros((n, 2), np.float32))
+    got_a = amax.cpu().numpy()[sample]
+    got_r = regret.cpu().numpy()[sample]
+    assert np.array_equal(got_a, r["argmax"][0::2]), (got_a, r["argmax"][0::2])
+    assert np.array_equal(got_r.view(np.uint32), r["regret"][0::2].view(np.uint32)), (
+        got_r, r["regret"][0::2])
+
+
 def test_maximum_hidden_size_bit_exact():
     """d = 2^20, the largest hidden size the call accepts: the copies reach
     their largest offsets (255 rows of 2 MB) and the K loop runs 16,384
