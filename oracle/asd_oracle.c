@@ -10,14 +10,17 @@
  *
  *   1. For every target logit row z_i the greedy token y*_i = argmax_v z_i(v)
  *      (Sec. 3.1, Eq. 1).  Ties go to the lowest index.
- *   2. For every draft block, Algorithm 1 (Sec. 3.2) in its own order:
- *      the B = 0 dispatch to exact greedy verification (Eq. 2); the mismatch
- *      indicator d_i (Eq. 5) and local regret r_i (Eq. 3); the remaining
- *      length q_i (Eq. 6); the cumulative regret C_i and count N_i (Eq. 8);
- *      the feasibility mask f_i (Sec. 3.3, Eq. 14, built from the gate of
- *      Eq. 7 and the constraints of Eqs. 9-11); the longest all-true prefix
- *      a (Eq. 12); the ledger update s' = s + C_a (Sec. 3.3, Eq. 13); and the
- *      recovery token y*_{a+1} or, when a = K, the bonus token y*_{K+1}.
+ *   2. For every draft block, its accepted length.  When the request's total
+ *      budget B is zero, the paper dispatches to exact greedy verification,
+ *      so the length is the strict prefix of Eq. 2.  Otherwise it is the
+ *      largest t in 0..K whose prefix x_{1:t} is feasible (Eq. 12), every
+ *      candidate t being checked directly against the definitions: the
+ *      mismatch indicator d_i (Eq. 5), the regret r_i (Eq. 3), the remaining
+ *      length q_i (Eq. 6), the running totals C_t and N_t (Eq. 8), the budget
+ *      (Eq. 9), the cap (Eq. 10) and the gate at every mismatch i <= t
+ *      (Eqs. 7 and 11).  Then the ledger update s' = s + C_a (Sec. 3.3,
+ *      Eq. 13) and the emitted token y*_{a+1}: the recovery token when a < K,
+ *      the bonus token y*_{K+1} when a = K (Sec. 3.3).
  *   3. The opportunity statistic of Eq. 4 (Sec. 3.1) from the per-row outputs.
  *   4. The commit of the emitted tokens that keeps the caches on the emitted
  *      sequence (Sec. 3.3).
@@ -128,88 +131,118 @@ void oracle_argmax_rows(const void *logits, int dtype, int64_t vocab,
         out[row] = (int32_t)oracle_row_argmax(logits, dtype, vocab, row);
 }
 
-/* ------------------------------------------------------------ Algorithm 1 */
+/* ------------------------------------------------- accepted length (Sec. 3.2) */
 
 /*
- * Algorithm 1 for one draft block of length K >= 0.
+ * Is the prefix x_{1:t} feasible (Sec. 3.2, Eqs. 9-11)?
  *
- * Inputs are the ones the algorithm requires:
+ * C_t and N_t are the sums of Eq. 8 over positions 1..t, formed here from
+ * scratch for this t: C_t in binary32 from +0, adding d_i r_i in position
+ * order (a match adds nothing, whatever its r_i), N_t as an integer count.
+ * The gate (Eqs. 7 and 11) must hold at every mismatch i <= t; it is decided
+ * as r_i <= g q_i in binary64, with q_i = K - i + 1 (Eq. 6), or q_i = 1 for
+ * the raw-gate variant.  A draft id outside the vocabulary is a mismatch that
+ * no prefix may contain.  A prefix that holds no mismatch spends nothing and
+ * is feasible (the first term of Eq. 14); one that holds a mismatch must also
+ * meet the budget (Eq. 9, decided as fl32(s + C_t) <= B) and the cap N_t <= M
+ * (Eq. 10).  d, x_valid and r are indexed from 0 (position i is entry i - 1).
+ */
+static int prefix_is_feasible(int32_t t, int32_t K, const uint8_t *d,
+                              const uint8_t *x_valid, const float *r,
+                              float B_total, float s, float g, int32_t M,
+                              int raw_gate)
+{
+    float C_t = 0.0f;
+    int64_t N_t = 0;
+    for (int32_t i = 1; i <= t; ++i) {
+        double q_i;
+        if (!d[i - 1])
+            continue;
+        if (!x_valid[i - 1])
+            return 0;
+        q_i = raw_gate ? 1.0 : (double)(K - i + 1);
+        if (!((double)r[i - 1] <= (double)g * q_i))
+            return 0;
+        C_t = C_t + r[i - 1];
+        N_t = N_t + 1;
+    }
+    if (N_t == 0)
+        return 1;
+    return (float)(s + C_t) <= B_total && N_t <= (int64_t)M;
+}
+
+/*
+ * The accepted length of one draft block of length K >= 0, with its emitted
+ * token and ledger update.
+ *
+ * Inputs:
  *   x[0..K-1]        the draft block x_1..x_K (token ids)
  *   x_valid[0..K-1]  1 if x_i is a vocabulary id (0 <= x_i < V), else 0
  *   y[0..K]          the target greedy tokens y*_1..y*_{K+1}
  *   z_y[0..K-1]      the target logits z_i(y*_i)
  *   z_x[0..K-1]      the target logits z_i(x_i) (not read where x_valid == 0)
- *   B_total, *s      the request state (B, s); *s is updated in place
+ *   B_total, *s      the request's ledger (B, s); *s is updated in place
  *   g, M             the local gate and the per-block exception cap
  *   raw_gate         nonzero: gate on r_i <= g (q_i read as 1)
- * Outputs: *a (accepted prefix length) and *next (recovery or bonus token);
+ * Outputs: *a_out (accepted length), *next_out (the emitted token y*_{a+1});
  * r_out[0..K-1] receives r_i when non-NULL.
+ *
+ * B = 0 is exact greedy verification with the ledger unchanged: a is the
+ * largest t with x_i = y*_i for every i <= t (Eq. 2).  Otherwise a is the
+ * largest feasible t (Eq. 12), and s' = s + C_a (Eq. 13) when the accepted
+ * prefix holds a mismatch (s is left untouched when it holds none).
  */
 void oracle_block(int32_t K, const int32_t *x, const uint8_t *x_valid,
                   const int32_t *y, const float *z_y, const float *z_x,
                   float B_total, float *s, float g, int32_t M, int raw_gate,
                   int32_t *a_out, int32_t *next_out, float *r_out)
 {
-    int32_t a;
+    size_t n = (size_t)(K > 0 ? K : 1);
+    uint8_t *d = (uint8_t *)malloc(n);
+    float *r = (float *)malloc(sizeof(float) * n);
+    int32_t a = 0;
 
-    /* Regret (Eq. 3) is reported for every draft position on both paths. */
-    float *r = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
-    uint8_t *d = (uint8_t *)malloc((size_t)(K > 0 ? K : 1));
-    for (int32_t i = 0; i < K; ++i) {
-        d[i] = (!x_valid[i] || x[i] != y[i]) ? 1 : 0;            /* Eq. 5 */
-        r[i] = x_valid[i] ? (z_y[i] - z_x[i]) : INFINITY;        /* Eq. 3 */
+    for (int32_t i = 1; i <= K; ++i) {
+        /* Eq. 5 on token ids; a non-vocabulary id equals no greedy token */
+        d[i - 1] = (x_valid[i - 1] && x[i - 1] == y[i - 1]) ? 0 : 1;
+        /* Eq. 3: one binary32 subtraction; +inf for a non-vocabulary id */
+        r[i - 1] = x_valid[i - 1] ? z_y[i - 1] - z_x[i - 1] : INFINITY;
         if (r_out)
-            r_out[i] = r[i];
+            r_out[i - 1] = r[i - 1];
     }
 
     if (B_total == 0.0f) {
-        /* B = 0: exact greedy verification (Eq. 2), state unchanged. */
-        a = 0;
-        while (a < K && x_valid[a] && x[a] == y[a])
-            ++a;
+        /* Eq. 2: the largest t whose drafts all equal the greedy tokens */
+        for (int32_t t = 0; t <= K; ++t) {
+            int all_equal = 1;
+            for (int32_t i = 1; i <= t; ++i)
+                if (d[i - 1])
+                    all_equal = 0;
+            if (all_equal)
+                a = t;
+        }
     } else {
-        int32_t *q = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K > 0 ? K : 1));
-        float *C = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
-        int64_t *N = (int64_t *)malloc(sizeof(int64_t) * (size_t)(K > 0 ? K : 1));
-        uint8_t *f = (uint8_t *)malloc((size_t)(K > 0 ? K : 1));
-        float C_prev = 0.0f;
-        int64_t N_prev = 0;
-
-        for (int32_t i = 0; i < K; ++i)
-            q[i] = raw_gate ? 1 : K - (i + 1) + 1;                /* Eq. 6 */
-
-        for (int32_t i = 0; i < K; ++i) {                         /* Eq. 8 */
-            /* d_i r_i adds nothing at a match (r_i there may be inf/NaN). */
-            C[i] = d[i] ? (C_prev + r[i]) : C_prev;
-            N[i] = N_prev + d[i];
-            C_prev = C[i];
-            N_prev = N[i];
-        }
-
-        for (int32_t i = 0; i < K; ++i) {                         /* Eq. 14 */
-            int gate = (double)r[i] <= (double)g * (double)q[i];  /* Eqs. 7, 11 */
-            int budget = (float)(*s + C[i]) <= B_total;           /* Eq. 9 */
-            int cap = N[i] <= (int64_t)M;                         /* Eq. 10 */
-            f[i] = x_valid[i] && (!d[i] || (gate && budget && cap));
-        }
-
-        a = 0;                   /* Eq. 12: longest all-true prefix of f */
-        while (a < K && f[a])
-            ++a;
-
-        if (a > 0 && N[a - 1] > 0)                                /* Eq. 13 */
-            *s = *s + C[a - 1];
-
-        free(q);
-        free(C);
-        free(N);
-        free(f);
+        float C_a = 0.0f;
+        int64_t N_a = 0;
+        /* Eq. 12: the largest feasible t */
+        for (int32_t t = 0; t <= K; ++t)
+            if (prefix_is_feasible(t, K, d, x_valid, r, B_total, *s, g, M,
+                                   raw_gate))
+                a = t;
+        /* Eq. 13 with the totals of Eq. 8 over the accepted prefix */
+        for (int32_t i = 1; i <= a; ++i)
+            if (d[i - 1]) {
+                C_a = C_a + r[i - 1];
+                N_a = N_a + 1;
+            }
+        if (N_a > 0)
+            *s = *s + C_a;
     }
 
     *a_out = a;
-    *next_out = y[a];   /* recovery y*_{a+1} if a < K, bonus y*_{K+1} if a = K */
-    free(r);
+    *next_out = y[a];   /* y*_{a+1}: recovery if a < K, bonus if a = K */
     free(d);
+    free(r);
 }
 
 /* ------------------------------------------------------- whole verifier call */
