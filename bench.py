@@ -19,7 +19,6 @@ the verification from their partials, all on this one GPU.
                                            # scaling rocprofv3 FETCH/WRITE_SIZE
 """
 import argparse
-import hashlib
 import json
 import os
 import re
@@ -36,8 +35,6 @@ METRIC = "verified logit rows/s + achieved HBM GB/s (B=256,K=16,V=151936 bf16)"
 PEAK_HBM_GBPS = 8000.0
 LLC_BYTES = 256 * 1024 * 1024            # MI355X last-level (Infinity) cache
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_03447_amd", "csrc", f)
-                  for f in ("asd_kernels.hip", "asd_plan.h", "asd_api.cpp")]
 
 
 def log(*a):
@@ -45,17 +42,11 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    """Hash of the library's sources with comments and whitespace removed, so that
-    an edit to a comment does not detach the counter profiles measured on the
-    same code."""
-    h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(p) as f:
-            text = f.read()
-        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-        text = re.sub(r"//[^\n]*", " ", text)
-        h.update(" ".join(text.split()).encode())
-    return h.hexdigest()[:16]
+    """Hash of the library's sources with comments and whitespace removed (the
+    hash the build embeds in the library), so that an edit to a comment does
+    not detach the counter profiles measured on the same code."""
+    from paper_2608_03447_amd.build import source_hash
+    return source_hash()
 
 
 def algorithmic_bytes(w) -> int:
@@ -72,6 +63,18 @@ def workload_tag(config: int, w) -> str:
     if w.blocks > 1:
         tag += "_seq%d" % w.blocks
     return tag
+
+
+PAPER_CONTEXT = ("The paper reports +3.05% to +15.26% fixed-workload tokens/s over matched strict "
+                 "speculative decoding on one NVIDIA L20 (Sec. 4, Table 2): end-to-end serving "
+                 "gains, context only, not comparable with this verifier-only measurement.")
+
+
+def traffic_note(tag: str, kernel: str = "asd_row_kernel") -> str:
+    """Where `traffic` comes from: it is not measured by the bench run itself."""
+    return ("profiles/%s_%s_pmc.md: rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE passes of this "
+            "workload on the same sources (hash checked), scaled by the plain-copy calibration; "
+            "not measured in this run" % (kernel, tag))
 
 
 def read_traffic(tag: str, source_hash: str, kernel: str = "asd_row_kernel"):
@@ -609,6 +612,7 @@ def main():
     if args.graph:
         tag += "_graph"
     traffic = read_traffic(tag, kernel_source_hash())
+    traffic_source = traffic_note(tag) if traffic else None
     metric = METRIC if (args.config == 3 and not args.shards and not args.opportunity
                         and not args.graph) else (
         "verified logit rows/s + achieved HBM GB/s (%s%s%s%s)" % (
@@ -617,7 +621,7 @@ def main():
             ", graph-captured rounds with commit" if args.graph else ""))
     call_roofline = {
         "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-        "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
+        "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic, "traffic_source": traffic_source,
         "algorithmic_bytes_per_launch": alg_bytes, "avg_launch_ms": ms_per_step,
         "timing": ("HIP events around each timed step, after a 512 MiB read-modify-write that "
                    "evicts the logits from the 256 MB last-level cache; " if cold else
@@ -627,7 +631,7 @@ def main():
         # The dominant kernel alone: the row kernel, timed live in this run.
         roofline = {"kernel": "asd_row_kernel", "bound": "hbm", "achieved": row_only["achieved"],
                     "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": row_only["frac"],
-                    "traffic": traffic,
+                    "traffic": traffic, "traffic_source": traffic_source,
                     "traffic_GBps": (traffic / (row_only["avg_launch_ms"] / 1e3) / 1e9
                                      if traffic else None),
                     "algorithmic_bytes_per_launch": row_only["algorithmic_bytes_per_launch"],
@@ -678,6 +682,7 @@ def main():
         "acceptance": acceptance,
         "torch_amax_same_logits_GBps": probe_gbps,
         "kernel_source_sha256_16": kernel_source_hash(),
+        "paper_context": PAPER_CONTEXT,
     }
     out["per_call"] = per_call
     out["practical_read"] = practical
@@ -764,6 +769,8 @@ def bench_lmhead(args, torch, asd, W):
     ok = bool(np.all(got[decided] == order[decided, 0]) and
               np.all(z.max(axis=1) - z[np.arange(16), got] <= 2 * bound))
     flops = 2.0 * rows * V * d
+    lm_tag = "%s_d%d" % (workload_tag(args.config, w), d)
+    lm_traffic = read_traffic(lm_tag, kernel_source_hash(), "asd_lmhead_kernel")
     out = {
         "metric": "verified logit rows/s, LM-head-fused (%s, d=%d)" % (w.name, d),
         "value": rows / (fused_ms / 1e3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
@@ -777,8 +784,10 @@ def bench_lmhead(args, torch, asd, W):
         "roofline": {"bound": "mfma", "achieved": flops / (fused_ms / 1e3) / 1e12,
                      "peak": 2500.0, "unit": "TFLOP/s",
                      "frac": flops / (fused_ms / 1e3) / 1e12 / 2500.0,
-                     "traffic": read_traffic("%s_d%d" % (workload_tag(args.config, w), d),
-                                             kernel_source_hash(), "asd_lmhead_kernel")},
+                     "traffic": lm_traffic,
+                     "traffic_source": traffic_note(lm_tag, "asd_lmhead_kernel")
+                     if lm_traffic else None},
+        "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(out), flush=True)
 

@@ -395,7 +395,9 @@ asd_status asd_read_probe(const void *buf, int64_t rows, int64_t row_bytes, uint
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 
-/* Library version string, e.g. "asd-mi355x 0.3.0 gfx950" (static storage). */
+/* Library version string (static storage), e.g.
+ * "asd-mi355x 0.4.0 gfx950 src 0123456789abcdef": the last word is a hash of
+ * the sources the library was built from (comments and whitespace ignored). */
 const char *asd_version(void);
 
 /*

@@ -11,14 +11,14 @@ import os
 
 import torch
 
-from .build import LIBRARY
+from .build import HASHED_SOURCES, LIBRARY, source_hash
 
 __all__ = ["asd_verify", "asd_verify_ws", "asd_verify_ex", "asd_shard_argmax",
            "asd_verify_partials", "asd_opportunity", "asd_commit", "asd_verify_commit",
            "asd_lmhead_verify", "asd_device_error", "asd_read_probe", "asd_workspace_bytes",
            "asd_status_string", "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16",
            "ASD_GATE_RAW", "ASD_DEVERR_NEGATIVE_K", "ASD_DEVERR_ROWS", "ASD_DEVERR_COMMIT",
-           "library_path"]
+           "library_path", "library_source_hash", "check_built_from_sources"]
 
 ASD_F32 = 0
 ASD_BF16 = 1
@@ -41,6 +41,22 @@ def library_path() -> str:
     return LIBRARY
 
 
+def library_source_hash(lib) -> str:
+    """The source hash a loaded library was built with (last word of asd_version)."""
+    return lib.asd_version().decode().split()[-1]
+
+
+def check_built_from_sources(lib, path=LIBRARY):
+    """Raise unless the library was built from the sources beside it (the hash
+    embedded by the build equals the hash of the current sources)."""
+    if not all(os.path.exists(p) for p in HASHED_SOURCES):
+        raise RuntimeError("the sources of %s are missing; cannot check the build" % path)
+    built, current = library_source_hash(lib), source_hash()
+    if built != current:
+        raise RuntimeError("%s was built from other sources (built %s, sources %s); run "
+                           "__graft_entry__.build() again" % (path, built, current))
+
+
 def _load():
     global _lib
     if _lib is not None:
@@ -49,6 +65,9 @@ def _load():
         raise RuntimeError("libasd.so is not built (%s); run __graft_entry__.build() first"
                            % LIBRARY)
     lib = ctypes.CDLL(LIBRARY)
+    lib.asd_version.argtypes = []
+    lib.asd_version.restype = ctypes.c_char_p
+    check_built_from_sources(lib, LIBRARY)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     common = [vp, ctypes.c_int, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.asd_verify.argtypes = common

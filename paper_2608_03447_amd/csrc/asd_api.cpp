@@ -519,7 +519,12 @@ const char* asd_status_string(asd_status status) {
     }
 }
 
-const char* asd_version(void) { return "asd-mi355x 0.3.0 gfx950"; }
+// The build passes the hash of the sources it compiled; the binding compares
+// it with the sources beside the library.
+#ifndef ASD_SOURCE_HASH
+#define ASD_SOURCE_HASH "unhashed"
+#endif
+const char* asd_version(void) { return "asd-mi355x 0.4.0 gfx950 src " ASD_SOURCE_HASH; }
 
 asd_status asd_release(void) {
     std::lock_guard<std::mutex> lock(g_mutex);
