@@ -46,7 +46,9 @@ enum {
     ASD_EDTYPE = 2,    /* unknown dtype; nothing launched */
     ASD_ENOMEM = 3,    /* workspace could not be allocated, or too small */
     ASD_EHIP = 4,      /* a HIP runtime call or kernel launch failed */
-    ASD_ECAPTURE = 5   /* the library workspace must grow while the stream is captured */
+    ASD_ECAPTURE = 5,  /* the library workspace must grow while the stream is captured */
+    ASD_ESCRATCH = 6   /* the call needs more workspace than asd_verify_static's fixed
+                          scratch holds; nothing launched */
 };
 
 /*
@@ -153,6 +155,36 @@ asd_status asd_verify_ws(const void *logits, asd_dtype dtype, int64_t vocab,
                          int32_t *out_accept_len, int32_t *out_next_token,
                          int32_t *out_argmax, float *out_regret, void *stream,
                          void *workspace, size_t workspace_bytes);
+
+/* Bytes of the fixed device scratch of asd_verify_static (4 MiB per device). */
+#define ASD_STATIC_SCRATCH_BYTES ((size_t)4 << 20)
+
+/*
+ * asd_verify_static -- asd_verify that allocates nothing, for callers that
+ * cannot allocate device memory: code under stream (graph) capture, tight
+ * serving loops, harnesses that forbid hipMalloc.
+ *
+ * Arguments and outputs are those of asd_verify, with the same results.  The
+ * call's workspace is a fixed device array of ASD_STATIC_SCRATCH_BYTES bytes
+ * that the library holds on every device it runs on until the process ends;
+ * the call never calls hipMalloc or hipFree.  A call whose workspace
+ * (asd_workspace_bytes) exceeds that size returns ASD_ESCRATCH with nothing
+ * launched: it needs 8 bytes per request, 8 per row, and 16 per vocabulary
+ * split of a row when rows are split (about 500,000 whole rows fit).
+ * Every call on a device shares that device's array, which keeps the last
+ * call's contents; nothing in it needs to start at zero or is carried from one
+ * call to the next.  Calls that may overlap on one device (different streams,
+ * or host threads without ordering) race on the array and must not be issued;
+ * calls in order on one stream are safe.  The first call on a device looks up
+ * the array's address.
+ */
+asd_status asd_verify_static(const void *logits, asd_dtype dtype, int64_t vocab,
+                             int32_t num_requests, int64_t total_rows,
+                             const int32_t *draft_tokens, const int32_t *block_lens,
+                             const int64_t *row_offsets, const float *tau,
+                             const int32_t *exc_cap, asd_budget *budget_inout,
+                             int32_t *out_accept_len, int32_t *out_next_token,
+                             int32_t *out_argmax, float *out_regret, void *stream);
 
 /* Flags of asd_verify_ex. */
 enum {

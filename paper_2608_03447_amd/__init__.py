@@ -13,7 +13,7 @@ import torch
 
 from .build import HASHED_SOURCES, LIBRARY, source_hash
 
-__all__ = ["asd_verify", "asd_verify_ws", "asd_verify_ex", "asd_shard_argmax",
+__all__ = ["asd_verify", "asd_verify_static", "asd_verify_ws", "asd_verify_ex", "asd_shard_argmax",
            "asd_verify_partials", "asd_opportunity", "asd_commit", "asd_verify_commit",
            "asd_lmhead_verify", "asd_device_error", "asd_read_probe", "asd_workspace_bytes",
            "asd_status_string", "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16",
@@ -26,6 +26,8 @@ ASD_GATE_RAW = 1            # asd_verify_ex flag: gate on r <= g instead of r / 
 ASD_DEVERR_NEGATIVE_K = 1   # device error word bits (asd_device_error)
 ASD_DEVERR_ROWS = 2
 ASD_DEVERR_COMMIT = 4
+ASD_ESCRATCH = 6            # status: the call needs more than asd_verify_static's scratch
+ASD_STATIC_SCRATCH_BYTES = 4 << 20
 _DTYPES = {torch.float32: ASD_F32, torch.bfloat16: ASD_BF16}
 
 _lib = None
@@ -72,6 +74,8 @@ def _load():
     common = [vp, ctypes.c_int, i64, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.asd_verify.argtypes = common
     lib.asd_verify.restype = ctypes.c_int
+    lib.asd_verify_static.argtypes = common
+    lib.asd_verify_static.restype = ctypes.c_int
     lib.asd_verify_ws.argtypes = common + [vp, sz]
     lib.asd_verify_ws.restype = ctypes.c_int
     lib.asd_verify_ex.argtypes = common[:-1] + [ctypes.c_uint32, vp, vp, sz]
@@ -215,6 +219,25 @@ def asd_verify(logits, draft_tokens, block_lens, tau, exc_cap, budget, *, row_of
     del keep
     if st != 0:
         raise AsdError(st, "asd_verify")
+    return acc, nxt
+
+
+def asd_verify_static(logits, draft_tokens, block_lens, tau, exc_cap, budget, *,
+                      row_offsets=None, out_accept_len=None, out_next_token=None,
+                      out_argmax=None, out_regret=None):
+    """``asd_verify`` with its workspace in the library's fixed per-device scratch
+    (``asd_verify_static`` of ``include/asd.h``): the call allocates nothing.
+    Calls that may overlap on one device race on that scratch."""
+    _check_logits(logits)
+    with torch.cuda.device(logits.device):
+        args, acc, nxt, keep = _marshal(logits.device, logits.shape[0], draft_tokens, block_lens,
+                                        tau, exc_cap, budget, row_offsets, out_accept_len,
+                                        out_next_token, out_argmax, out_regret)
+        st = _load().asd_verify_static(ctypes.c_void_p(logits.data_ptr()),
+                                       _DTYPES[logits.dtype], logits.shape[1], *args)
+    del keep
+    if st != 0:
+        raise AsdError(st, "asd_verify_static")
     return acc, nxt
 
 

@@ -13,6 +13,9 @@
 
 namespace asd {
 
+static_assert(kStaticScratchBytes == ASD_STATIC_SCRATCH_BYTES,
+              "the fixed scratch size of the header and the kernels must agree");
+
 namespace {
 
 size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
@@ -295,6 +298,27 @@ asd_status asd_verify_ex(const void* logits, asd_dtype dtype, int64_t vocab,
                    (flags & ASD_GATE_RAW) != 0);
 }
 
+asd_status asd_verify_static(const void* logits, asd_dtype dtype, int64_t vocab,
+                             int32_t num_requests, int64_t total_rows,
+                             const int32_t* draft_tokens, const int32_t* block_lens,
+                             const int64_t* row_offsets, const float* tau,
+                             const int32_t* exc_cap, asd_budget* budget_inout,
+                             int32_t* out_accept_len, int32_t* out_next_token,
+                             int32_t* out_argmax, float* out_regret, void* stream) {
+    asd_status st = check_args(logits, dtype, vocab, num_requests, total_rows, draft_tokens,
+                               block_lens, tau, exc_cap, budget_inout, out_accept_len,
+                               out_next_token);
+    if (st != ASD_OK || num_requests == 0) return st;
+    Plan plan;
+    if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
+    if (plan.ws_bytes > kStaticScratchBytes) return ASD_ESCRATCH;
+    void* ws = nullptr;
+    if (static_scratch_address(&ws) != hipSuccess) return ASD_EHIP;
+    return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
+                   row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
+                   out_argmax, out_regret, (hipStream_t)stream, plan, ws);
+}
+
 asd_status asd_device_error(uint32_t* out_word, int32_t clear, void* stream) {
     if (!out_word) return ASD_EINVAL;
     hipStream_t s = (hipStream_t)stream;
@@ -515,6 +539,9 @@ const char* asd_status_string(asd_status status) {
         case ASD_ENOMEM: return "ASD_ENOMEM: workspace allocation failed or too small";
         case ASD_EHIP: return "ASD_EHIP: HIP runtime error";
         case ASD_ECAPTURE: return "ASD_ECAPTURE: workspace must grow during stream capture";
+        case ASD_ESCRATCH:
+            return "ASD_ESCRATCH: the call needs more workspace than the fixed scratch of "
+                   "asd_verify_static holds";
         default: return "ASD: unknown status";
     }
 }

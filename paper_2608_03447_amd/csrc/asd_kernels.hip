@@ -25,9 +25,37 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <map>
+#include <mutex>
+
 #include "asd_plan.h"
 
+// Workspace of asd_verify_static, for callers that cannot allocate: one fixed
+// array per device, held until the process ends.  In host code its name is
+// only a stand-in for the symbol, not a device address; host code uses the
+// address static_scratch_address returns for the current device.
+static __device__ __align__(256) unsigned char scratch[asd::kStaticScratchBytes];
+
 namespace asd {
+
+hipError_t static_scratch_address(void** ptr) {
+    static std::mutex m;
+    static std::map<int, void*> by_device;   // each device holds its own copy
+    int device = 0;
+    hipError_t err = hipGetDevice(&device);
+    if (err != hipSuccess) return err;
+    std::lock_guard<std::mutex> lock(m);
+    auto it = by_device.find(device);
+    if (it == by_device.end()) {
+        void* p = nullptr;
+        err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (err != hipSuccess) return err;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        it = by_device.emplace(device, p).first;
+    }
+    *ptr = it->second;
+    return hipSuccess;
+}
 
 // Sticky error word of this device: the kernels OR in kErr* bits when they meet
 // data that the verifier reads in a defined but unusual way.

@@ -42,6 +42,14 @@ constexpr uint32_t kErrCommit = 4u;      // a verified request whose tokens were
 // device current at the call.
 hipError_t error_word_address(uint32_t** ptr);
 
+// Size of the fixed per-device workspace of asd_verify_static (the value of
+// ASD_STATIC_SCRATCH_BYTES).
+constexpr size_t kStaticScratchBytes = (size_t)4 << 20;
+
+// Device address of that workspace on the device current at the call, looked
+// up once per device and cached.
+hipError_t static_scratch_address(void** ptr);
+
 constexpr uint32_t kMismatchBit = 0x80000000u;
 constexpr uint32_t kBadDraftBit = 0x40000000u;
 constexpr uint32_t kArgmaxMask = 0x3fffffffu;
