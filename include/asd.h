@@ -306,7 +306,7 @@ asd_status asd_verify_partials(const asd_row_partial *partials, int32_t num_shar
  *
  * draft_tokens, block_lens, row_offsets, num_requests, total_rows, vocab
  *                 as for asd_verify (the batch that was verified); row_offsets
- *                 may be NULL (packed layout) only up to 1024 requests.
+ *                 may be NULL (packed layout) for any number of requests.
  * row_argmax      int32 [total_rows]: the out_argmax of asd_verify on the batch.
  * row_regret      float [total_rows]: the out_regret of asd_verify on the batch.
  * taus            float [num_taus] (raw regret thresholds); ps int32 [num_ps],
@@ -332,7 +332,7 @@ asd_status asd_opportunity(const int32_t *draft_tokens, const int32_t *row_argma
  *
  * draft_tokens, block_lens, row_offsets, num_requests, total_rows
  *                 as for the asd_verify call (row_offsets may be NULL, the packed
- *                 layout, only up to 1024 requests).
+ *                 layout, for any number of requests).
  * accept_len, next_token   the outputs of that call.
  * tokens          int32 [num_requests][capacity]: entries
  *                 [seq_len_i, seq_len_i + a_i + 1) of row i are written.

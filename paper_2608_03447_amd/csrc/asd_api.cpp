@@ -425,7 +425,6 @@ asd_status asd_opportunity(const int32_t* draft_tokens, const int32_t* row_argma
     if (!draft_tokens || !row_argmax || !row_regret || !block_lens || !taus || !ps || !counts ||
         !mismatches)
         return ASD_EINVAL;
-    if (!row_offsets && num_requests > kWaveOffsetsMaxRequests) return ASD_EINVAL;
     return launch_opportunity(draft_tokens, row_argmax, row_regret, vocab, num_requests,
                               total_rows, block_lens, row_offsets, taus, num_taus, ps, num_ps,
                               (unsigned long long*)counts, (unsigned long long*)mismatches,
@@ -444,7 +443,6 @@ asd_status asd_commit(const int32_t* draft_tokens, const int32_t* block_lens,
     if (num_requests == 0) return ASD_OK;
     if (!draft_tokens || !block_lens || !accept_len || !next_token || !tokens || !seq_len)
         return ASD_EINVAL;
-    if (!row_offsets && num_requests > kWaveOffsetsMaxRequests) return ASD_EINVAL;
     if (capacity > INT64_MAX / num_requests) return ASD_EINVAL;
     return launch_commit(draft_tokens, block_lens, row_offsets, num_requests, total_rows,
                          accept_len, next_token, tokens, capacity, seq_len, out_committed,

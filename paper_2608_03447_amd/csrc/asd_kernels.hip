@@ -333,6 +333,49 @@ __device__ void write_packed_offsets(int32_t num_requests, const int32_t* __rest
     }
 }
 
+// Row offsets of one workgroup's requests [first, first + count), count <=
+// kScanThreads, into s_off: row_offsets[i] when given, else the packed layout
+// o_i = sum_{j<i} (max(K_j, 0) + 1).  For the packed layout the whole workgroup
+// sums the row counts of the requests before `first`, then scans its own, so
+// no request count is too large and nothing is written to global memory.
+// Ends with a barrier.
+__device__ void block_offsets(int32_t num_requests, const int32_t* __restrict__ block_lens,
+                              const int64_t* __restrict__ row_offsets, int64_t first, int count,
+                              int64_t* s_off) {
+    __shared__ long long s_before[kWaves];
+    __shared__ long long s_mine[kWaves];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (row_offsets) {
+        if (tid < count) s_off[tid] = row_offsets[first + tid];
+        __syncthreads();
+        return;
+    }
+    long long before = 0;
+    for (int64_t j = tid; j < first; j += blockDim.x) {
+        const int32_t K = block_lens[j];
+        before += (long long)(K > 0 ? K : 0) + 1;
+    }
+    const int32_t Km = tid < count ? block_lens[first + tid] : 0;
+    const long long mine = tid < count ? (long long)(Km > 0 ? Km : 0) + 1 : 0;
+    long long incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const long long t = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += t;
+        before += __shfl_xor(before, off, 64);
+    }
+    if (lane == 63) s_mine[wave] = incl;
+    if (lane == 0) s_before[wave] = before;
+    __syncthreads();
+    long long base = 0, earlier = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+        base += s_before[w];
+        earlier += (w < wave) ? s_mine[w] : 0;
+    }
+    if (tid < count) s_off[tid] = base + earlier + incl - mine;
+    __syncthreads();
+}
+
 // Where one lane's share of a tile lies: 16-byte vectors [v0, v1) of the row's
 // aligned middle, nfull whole groups of kGroupVecs vectors, then a partial one.
 struct TileSpan {
@@ -928,31 +971,22 @@ __global__ __launch_bounds__(kScanThreads) void asd_opportunity_kernel(
     int64_t total_rows, const int32_t* __restrict__ block_lens,
     const int64_t* __restrict__ row_offsets, const float* __restrict__ taus, int32_t num_taus,
     const int32_t* __restrict__ ps, int32_t num_ps, unsigned long long* __restrict__ counts,
-    unsigned long long* __restrict__ mismatches) {
+    unsigned long long* __restrict__ mismatches, int per_block) {
     __shared__ uint32_t s_counts[kMaxOpportunityPairs];
     __shared__ uint32_t s_mism;
+    __shared__ int64_t s_off[kScanThreads];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int pairs = num_taus * num_ps;
     for (int k = tid; k < pairs; k += kScanThreads) s_counts[k] = 0u;
     if (tid == 0) s_mism = 0u;
-    __syncthreads();
+    const int64_t first = (int64_t)blockIdx.x * per_block;
+    const int count = (int)min((int64_t)per_block, (int64_t)num_requests - first);
+    block_offsets(num_requests, block_lens, row_offsets, first, count, s_off);   // + barrier
 
-    const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
-    if (i < num_requests) {
+    for (int kq = wave; kq < count; kq += kScanThreads / 64) {    // wave-uniform
+        const int64_t i = first + kq;
         const int32_t K = block_lens[i];
-        int64_t o;
-        if (row_offsets) {
-            o = row_offsets[i];
-        } else {                                      // packed: sum the earlier blocks
-            long long part = 0;
-            for (int64_t j = lane; j < i; j += 64) {
-                const int32_t Kj = block_lens[j];
-                part += (long long)(Kj > 0 ? Kj : 0) + 1;
-            }
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
-            o = part;
-        }
+        const int64_t o = s_off[kq];
         if (K >= 0 && o >= 0 && o + (int64_t)K < total_rows) {
             // Chunks from the block's end: `carry` = greedy run starting at the
             // first position after the chunk.
@@ -1010,48 +1044,42 @@ __global__ __launch_bounds__(kScanThreads) void asd_opportunity_kernel(
 
 // The commit after verification: request i appends its emitted tokens x_1..x_a
 // and y*_{a+1} to its token buffer at its committed length and advances that
-// length (the extent the target and draft caches keep) by a + 1.  One
-// wavefront per request, lanes writing consecutive tokens.
+// length (the extent the target and draft caches keep) by a + 1.  Each
+// workgroup takes `per_block` consecutive requests, one wavefront per request
+// at a time, lanes writing consecutive tokens.
 __global__ __launch_bounds__(kScanThreads) void asd_commit_kernel(
     const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ block_lens,
     const int64_t* __restrict__ row_offsets, int32_t num_requests, int64_t total_rows,
     const int32_t* __restrict__ accept_len, const int32_t* __restrict__ next_token,
     int32_t* __restrict__ tokens, int64_t capacity, int64_t* __restrict__ seq_len,
-    int32_t* __restrict__ committed) {
+    int32_t* __restrict__ committed, int per_block) {
+    __shared__ int64_t s_off[kScanThreads];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
-    if (i >= num_requests) return;
-    const int32_t K_given = block_lens[i];
-    const int32_t K = K_given > 0 ? K_given : 0;      // a negative K is read as 0
-    int64_t o;
-    if (row_offsets) {
-        o = row_offsets[i];
-    } else {                                          // packed: sum the earlier blocks
-        long long part = 0;
-        for (int64_t j = lane; j < i; j += 64) {
-            const int32_t Kj = block_lens[j];
-            part += (long long)(Kj > 0 ? Kj : 0) + 1;
+    const int64_t first = (int64_t)blockIdx.x * per_block;
+    const int count = (int)min((int64_t)per_block, (int64_t)num_requests - first);
+    block_offsets(num_requests, block_lens, row_offsets, first, count, s_off);
+    for (int k = wave; k < count; k += kScanThreads / 64) {       // wave-uniform
+        const int64_t i = first + k;
+        const int32_t K_given = block_lens[i];
+        const int32_t K = K_given > 0 ? K_given : 0;  // a negative K is read as 0
+        const int64_t o = s_off[k];
+        const int32_t a = accept_len[i];
+        const int32_t next = next_token[i];
+        const int64_t L = seq_len[i];
+        const bool rows_ok = o >= 0 && o + (int64_t)K < total_rows;
+        const bool ok = rows_ok && next >= 0 && L >= 0 && a >= 0 && a <= K &&
+                        L + (int64_t)a + 1 <= capacity;
+        if (ok) {
+            int32_t* dst = tokens + i * capacity + L;
+            for (int64_t j = lane; j <= a; j += 64) dst[j] = j < a ? draft_tokens[o + j] : next;
         }
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
-        o = part;
-    }
-    const int32_t a = accept_len[i];
-    const int32_t next = next_token[i];
-    const int64_t L = seq_len[i];
-    const bool rows_ok = o >= 0 && o + (int64_t)K < total_rows;
-    const bool ok = rows_ok && next >= 0 && L >= 0 && a >= 0 && a <= K &&
-                    L + (int64_t)a + 1 <= capacity;
-    if (ok) {
-        int32_t* dst = tokens + i * capacity + L;
-        for (int64_t j = lane; j <= a; j += 64) dst[j] = j < a ? draft_tokens[o + j] : next;
-    }
-    if (lane == 0) {
-        if (ok) seq_len[i] = L + (int64_t)a + 1;
-        if (committed) committed[i] = ok ? a + 1 : 0;
-        const uint32_t err = (K_given < 0 ? kErrNegativeK : 0u) | (rows_ok ? 0u : kErrRows) |
-                             (rows_ok && next >= 0 && !ok ? kErrCommit : 0u);
-        if (err) atomicOr(&asd_error_word, err);
+        if (lane == 0) {
+            if (ok) seq_len[i] = L + (int64_t)a + 1;
+            if (committed) committed[i] = ok ? a + 1 : 0;
+            const uint32_t err = (K_given < 0 ? kErrNegativeK : 0u) | (rows_ok ? 0u : kErrRows) |
+                                 (rows_ok && next >= 0 && !ok ? kErrCommit : 0u);
+            if (err) atomicOr(&asd_error_word, err);
+        }
     }
 }
 
@@ -1458,17 +1486,25 @@ hipError_t launch_verify_partials(const void* partials, int num_shards, int64_t 
     return launch_scan(A, true, stream);
 }
 
+// Requests per workgroup of the commit and opportunity kernels: one per
+// wavefront while the packed layout's per-workgroup prefix sums stay short
+// (at most 8,192 requests before a workgroup), else 64, so that those sums
+// total about n^2 / 128 loads.
+static int requests_per_block(int32_t num_requests, const int64_t* row_offsets) {
+    return (row_offsets || num_requests <= 8192) ? kScanThreads / 64 : 64;
+}
+
 hipError_t launch_opportunity(const int32_t* draft_tokens, const int32_t* row_argmax,
                               const float* row_regret, int64_t vocab, int32_t num_requests,
                               int64_t total_rows, const int32_t* block_lens,
                               const int64_t* row_offsets, const float* taus, int32_t num_taus,
                               const int32_t* ps, int32_t num_ps, unsigned long long* counts,
                               unsigned long long* mismatches, hipStream_t stream) {
-    const unsigned blocks =
-        (unsigned)((num_requests + kScanThreads / 64 - 1) / (kScanThreads / 64));
+    const int per_block = requests_per_block(num_requests, row_offsets);
+    const unsigned blocks = (unsigned)((num_requests + per_block - 1) / per_block);
     asd_opportunity_kernel<<<blocks, kScanThreads, 0, stream>>>(
         draft_tokens, row_argmax, row_regret, vocab, num_requests, total_rows, block_lens,
-        row_offsets, taus, num_taus, ps, num_ps, counts, mismatches);
+        row_offsets, taus, num_taus, ps, num_ps, counts, mismatches, per_block);
     return hipGetLastError();
 }
 
@@ -1477,11 +1513,11 @@ hipError_t launch_commit(const int32_t* draft_tokens, const int32_t* block_lens,
                          const int32_t* accept_len, const int32_t* next_token, int32_t* tokens,
                          int64_t capacity, int64_t* seq_len, int32_t* committed,
                          hipStream_t stream) {
-    const unsigned blocks =
-        (unsigned)((num_requests + kScanThreads / 64 - 1) / (kScanThreads / 64));
+    const int per_block = requests_per_block(num_requests, row_offsets);
+    const unsigned blocks = (unsigned)((num_requests + per_block - 1) / per_block);
     asd_commit_kernel<<<blocks, kScanThreads, 0, stream>>>(
         draft_tokens, block_lens, row_offsets, num_requests, total_rows, accept_len, next_token,
-        tokens, capacity, seq_len, committed);
+        tokens, capacity, seq_len, committed, per_block);
     return hipGetLastError();
 }
 

@@ -191,7 +191,7 @@ def _commit(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(cap=0), 1), (dict(nreq=-1), 1), (dict(nreq=3, rows=2), 1), (dict(draft=None), 1),
     (dict(lens=None), 1), (dict(acc=None), 1), (dict(nxt=None), 1), (dict(tok=None), 1),
-    (dict(sl=None), 1), (dict(nreq=1025, rows=2000), 1), (dict(cap=1 << 62, nreq=4, rows=4), 1),
+    (dict(sl=None), 1), (dict(cap=1 << 62, nreq=4, rows=4), 1),
 ])
 def test_commit_rejects_invalid_arguments(kw, status):
     assert _commit(**kw) == status

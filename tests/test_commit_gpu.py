@@ -200,3 +200,93 @@ def test_graph_captured_rounds_match_eager_and_oracle(fused):
         for a, b in zip(got, eager):
             assert np.array_equal(a.view(np.uint32) if a.dtype == np.float32 else a,
                                   b.view(np.uint32) if b.dtype == np.float32 else b), replay
+
+
+def test_checkpoint_resume_across_sessions_is_bit_identical(tmp_path):
+    """Workload 1's 64 sequential rounds (verify and commit, asd_verify_commit)
+    run as two sessions: after 32 rounds the request state -- the ledger
+    (B, s) of Sec. 3.2 and the committed tokens and length of Sec. 3.3 -- is
+    copied to the host and saved to a file, the library's workspaces are
+    released and every device buffer is dropped; a second session loads the
+    file into fresh device buffers and runs the other 32 rounds.  The result
+    equals the uninterrupted 64-round run and the oracle's verify then commit,
+    bit for bit."""
+    w = W.make_config(1)
+    n = w.rows_per_call
+    capacity = w.blocks * (int(w.block_lens.max()) + 1)
+    logits_all, draft_all = w.logits, w.draft_tokens
+
+    def session(first, last, ledger, tokens, seq_len):
+        lg = t(logits_all[first * n:last * n])
+        dr = t(draft_all[first * n:last * n])
+        lens, tau, cap = t(w.block_lens), t(w.tau), t(w.exc_cap)
+        budget, tok, sl = t(ledger), t(tokens), t(seq_len)
+        for b in range(last - first):
+            asd.asd_verify_commit(lg[b * n:(b + 1) * n], dr[b * n:(b + 1) * n], lens, tau, cap,
+                                  budget, tok, sl)
+        torch.cuda.synchronize()
+        return budget.cpu().numpy(), tok.cpu().numpy(), sl.cpu().numpy()
+
+    ledger0 = w.budget.copy()
+    tokens0 = np.zeros((1, capacity), np.int32)
+    seq0 = np.zeros(1, np.int64)
+    print("case checkpoint/resume: workload 1, 64 rounds uninterrupted", flush=True)
+    whole = session(0, w.blocks, ledger0, tokens0, seq0)
+
+    print("case checkpoint/resume: 32 rounds, save, release, 32 rounds", flush=True)
+    first = session(0, 32, ledger0, tokens0, seq0)
+    path = tmp_path / "asd_state.npz"
+    np.savez(path, ledger=first[0], tokens=first[1], seq_len=first[2])
+    del first
+    torch.cuda.synchronize()
+    asd.asd_release()
+    torch.cuda.empty_cache()
+    with np.load(path) as f:
+        state = (f["ledger"].copy(), f["tokens"].copy(), f["seq_len"].copy())
+    resumed = session(32, w.blocks, *state)
+
+    ledger = ledger0.copy()
+    r_tok, r_sl = tokens0.copy(), seq0.copy()
+    for b in range(w.blocks):
+        lg, dr = w.call(b)
+        r = oracle.verify(lg, dr, w.block_lens, w.tau, w.exc_cap, ledger)
+        ledger = r["budget"]
+        r_tok, r_sl, _ = oracle.commit(dr, w.block_lens, r["accept_len"], r["next_token"],
+                                       r_tok, r_sl)
+    for got in (whole, resumed):
+        assert np.array_equal(got[0].view(np.uint32), ledger.view(np.uint32))
+        assert np.array_equal(got[1], r_tok)
+        assert np.array_equal(got[2], r_sl)
+    assert ledger[0, 1] > 0 and r_sl[0] > w.blocks      # exceptions were accepted
+
+
+@pytest.mark.parametrize("num_requests", [3000, 8193, 70000])
+def test_commit_packed_layout_any_request_count(num_requests):
+    """asd_commit with row_offsets NULL at batch sizes above the 1,024 that
+    one wavefront per request can sum on its own: against the oracle, with
+    negative and zero K, accepted lengths out of range, unverified requests
+    and tokens that do not fit."""
+    rng = np.random.default_rng(num_requests)
+    n = num_requests
+    lens = rng.integers(-1, 7, n).astype(np.int32)
+    k = np.maximum(lens, 0)
+    rows = int(np.sum(k + 1))
+    draft = rng.integers(0, 1000, rows).astype(np.int32)
+    acc = np.minimum(rng.integers(0, 8, n), k).astype(np.int32)
+    acc[rng.random(n) < 0.01] = 9                                 # outside [0, K]
+    nxt = rng.integers(0, 1000, n).astype(np.int32)
+    nxt[rng.random(n) < 0.02] = -1                                # not verified
+    capacity = 12
+    start = rng.integers(0, 6, n).astype(np.int64)
+    start[rng.random(n) < 0.05] = capacity - 2                     # may not fit
+    tokens0 = rng.integers(-5, 5, size=(n, capacity)).astype(np.int32)
+    print("case commit packed: %d requests, %d rows" % (n, rows), flush=True)
+    tok, sl = t(tokens0.copy()), t(start.copy())
+    done = torch.empty(n, dtype=torch.int32, device=DEV)
+    asd.asd_commit(t(draft), t(lens), t(acc), t(nxt), tok, sl, out_committed=done)
+    torch.cuda.synchronize()
+    r_tok, r_sl, r_done = oracle.commit(draft, lens, acc, nxt, tokens0, start)
+    assert np.array_equal(tok.cpu().numpy(), r_tok)
+    assert np.array_equal(sl.cpu().numpy(), r_sl)
+    assert np.array_equal(done.cpu().numpy(), r_done)
+    assert (r_done == 0).any() and (r_done > 1).any()

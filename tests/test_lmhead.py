@@ -127,48 +127,76 @@ def test_nonfinite_and_negative_rows_bit_exact(rows, vocab, d):
     assert not bad, "differs in %s: %s" % (bad, describe(g, r))
 
 
-def test_full_size_sampled_rows_bit_exact():
-    """The headline batch at full size in the launch configuration the bench
-    times: 4,352 rows x d 5,120 x V 151,936, exact-regime inputs made on the
-    device.  For sampled draft rows, the oracle forms the exact logits (the
-    weights copied back in chunks) and verifies each as a one-position block;
-    the row's argmax and regret must match bit for bit."""
+# The three launches the bench times: the headline batch at d = 5,120 and at
+# d = 4,096, and workload 5's ragged rows at d = 7,168 with V = 129,280.
+BENCH_SHAPES = [(3, 5120), (3, 4096), (5, 7168)]
+
+
+@pytest.mark.parametrize("config,d", BENCH_SHAPES)
+def test_full_size_every_output_bit_exact(config, d):
+    """Every row and every request of a benched launch, exact regime.  Hidden
+    states in {-2..2} and weights in {-1, -1/2, 0, 1/2, 1} are drawn on the
+    device; the oracle forms all R x V logits exactly on the host (weights
+    copied back in chunks), drafts are drawn from those logits (greedy token,
+    runner-up or uniform), and the workload's own requests, gates, caps and
+    budgets are verified.  Every per-row argmax and regret and every request's
+    accepted length, next token and ledger must match bit for bit."""
     import torch
     import paper_2608_03447_amd as asd
+    from asd_gpu import describe, mismatches
     dev = torch.device("cuda:0")
-    w = W.make_config(3)
-    rows, vocab, d = w.rows_per_call, w.vocab, 5120
-    g = torch.Generator(device=dev).manual_seed(77)
+    w = W.make_config(config)
+    rows, vocab = w.rows_per_call, w.vocab
+    print("case lmhead full size: workload %d, %d rows x d %d x V %d" % (config, rows, d, vocab),
+          flush=True)
+    g = torch.Generator(device=dev).manual_seed(7700 + d)
     hidden = torch.randint(-2, 3, (rows, d), generator=g, device=dev).to(torch.bfloat16)
     weight = (torch.randint(-2, 3, (vocab, d), generator=g, device=dev).to(torch.float32) / 2.0
               ).to(torch.bfloat16)
-    draft = torch.from_numpy(w.draft_tokens).to(dev)
+    h_bits = hidden.view(torch.int16).cpu().numpy().view(np.uint16)
+    z = np.empty((rows, vocab), np.float32)
+    for c in range(0, vocab, 8192):
+        z[:, c:c + 8192] = oracle.lmhead_logits(
+            h_bits, weight[c:c + 8192].view(torch.int16).cpu().numpy().view(np.uint16))
+    rng = np.random.default_rng(d + config)
+    top = np.argmax(z, axis=1)
+    at_top = z[np.arange(rows), top].copy()
+    z[np.arange(rows), top] = -np.inf           # the runner-up: greatest other column
+    second = np.argmax(z, axis=1)
+    z[np.arange(rows), top] = at_top
+    u = rng.random(rows)
+    draft = np.where(u < 0.6, top, np.where(u < 0.9, second, rng.integers(0, vocab, rows)))
+    draft = draft.astype(np.int32)
+    draft[rng.random(rows) < 0.01] = vocab + 5            # outside the vocabulary
+    budget = w.budget.copy()
+    got = _run_device(hidden, weight, draft, w, budget)
+    ref = oracle.verify(z, draft, w.block_lens, w.tau, w.exc_cap, budget, w.row_offsets)
+    accepted_mismatch = (ref["budget"][:, 1] != budget[:, 1]).sum()
+    print("  oracle: mean a %.2f, %d requests spent budget" % (ref["accept_len"].mean(),
+                                                               accepted_mismatch), flush=True)
+    assert accepted_mismatch > 0
+    bad = mismatches(got, ref)
+    assert not bad, "differs in %s: %s" % (bad, describe(got, ref))
+
+
+def _run_device(hidden, weight, draft, w, budget):
+    """asd_lmhead_verify on device tensors with a workload's requests."""
+    import torch
+    import paper_2608_03447_amd as asd
+    dev = hidden.device
+    rows = hidden.shape[0]
+    tb = torch.from_numpy(budget.copy()).to(dev)
     amax = torch.full((rows,), -7, dtype=torch.int32, device=dev)
     regret = torch.full((rows,), float("nan"), dtype=torch.float32, device=dev)
-    print("case lmhead full size %d x %d x %d" % (rows, d, vocab), flush=True)
-    asd.asd_lmhead_verify(hidden, weight, draft, torch.from_numpy(w.block_lens).to(dev),
-                          torch.from_numpy(w.tau).to(dev), torch.from_numpy(w.exc_cap).to(dev),
-                          torch.from_numpy(w.budget.copy()).to(dev), out_argmax=amax,
-                          out_regret=regret)
-    torch.cuda.synchronize()
-    rng = np.random.default_rng(5)
-    k = w.block_lens[0]
-    sample = np.sort(rng.choice(rows // (k + 1), 12, replace=False)) * (k + 1) + rng.integers(0, k, 12)
-    h_bits = hidden[torch.from_numpy(sample).to(dev)].view(torch.int16).cpu().numpy().view(np.uint16)
-    z = np.concatenate([oracle.lmhead_logits(
-        h_bits, weight[c:c + 16384].view(torch.int16).cpu().numpy().view(np.uint16))
-        for c in range(0, vocab, 16384)], axis=1)
-    # each sampled row as its draft row of a one-position block (its copy as the bonus row)
-    pairs = np.repeat(z, 2, axis=0)
-    dr = np.repeat(w.draft_tokens[sample], 2).astype(np.int32)
-    n = len(sample)
-    r = oracle.verify(pairs, dr, np.ones(n, np.int32), 1.0, 1,
-                      np.zeros((n, 2), np.float32))
-    got_a = amax.cpu().numpy()[sample]
-    got_r = regret.cpu().numpy()[sample]
-    assert np.array_equal(got_a, r["argmax"][0::2]), (got_a, r["argmax"][0::2])
-    assert np.array_equal(got_r.view(np.uint32), r["regret"][0::2].view(np.uint32)), (
-        got_r, r["regret"][0::2])
+    offs = None if w.row_offsets is None else torch.from_numpy(w.row_offsets).to(dev)
+    acc, nxt = asd.asd_lmhead_verify(
+        hidden, weight, torch.from_numpy(draft).to(dev), torch.from_numpy(w.block_lens).to(dev),
+        torch.from_numpy(w.tau).to(dev), torch.from_numpy(w.exc_cap).to(dev), tb,
+        row_offsets=offs, out_argmax=amax, out_regret=regret)
+    torch.cuda.synchronize(dev)
+    return {"accept_len": acc.cpu().numpy(), "next_token": nxt.cpu().numpy(),
+            "argmax": amax.cpu().numpy(), "regret": regret.cpu().numpy(),
+            "budget": tb.cpu().numpy()}
 
 
 def test_maximum_hidden_size_bit_exact():

@@ -44,8 +44,12 @@ def test_opportunity_matches_oracle_on_workloads(cfg):
     assert m > 0 and counts[-1, 1] > 0
 
 
-@pytest.mark.parametrize("num_requests", [1, 3, 4, 5, 1023, 1024, 3000])
-def test_opportunity_offsets_across_workgroups_and_accumulation(num_requests):
+@pytest.mark.parametrize("num_requests,explicit", [
+    (1, False), (3, False), (4, False), (5, False), (1023, False), (1024, False), (1025, False),
+    (3000, False), (3000, True), (8193, False), (70000, False), (70000, True)])
+def test_opportunity_offsets_across_workgroups_and_accumulation(num_requests, explicit):
+    """Packed (row_offsets NULL) or explicit offsets, from one request to 70,000:
+    above 8,192 packed requests each workgroup takes 64 requests."""
     rng = np.random.default_rng(num_requests)
     vocab = 300
     lens = rng.integers(0, 14, num_requests).astype(np.int32)
@@ -53,9 +57,11 @@ def test_opportunity_offsets_across_workgroups_and_accumulation(num_requests):
     y = rng.integers(0, vocab, rows).astype(np.int32)
     draft = np.where(rng.random(rows) < 0.7, y, rng.integers(-1, vocab + 1, rows)).astype(np.int32)
     regret = rng.choice(np.array([0.0, 0.25, 1.0, 3.0, np.inf, np.nan], np.float32), rows)
-    # packed offsets up to 1,024 requests; explicit ones above
-    offs = None if num_requests <= 1024 else np.concatenate(
+    offs = None if not explicit else np.concatenate(
         [[0], np.cumsum(lens.astype(np.int64) + 1)[:-1]])
+    print("case opportunity: %d requests, %s offsets" % (num_requests,
+                                                         "explicit" if explicit else "packed"),
+          flush=True)
     counts, m = gpu_counts(draft, y, regret, vocab, lens, TAUS, PS, row_offsets=offs, repeat=2)
     ref_c, ref_m = oracle.opportunity(draft, y, regret, vocab, lens, TAUS, PS)
     assert m == 2 * ref_m and np.array_equal(counts, 2 * ref_c)
@@ -75,14 +81,6 @@ def test_opportunity_long_blocks_cross_64_position_chunks():
         counts, m = gpu_counts(draft, y, regret, vocab, lens, TAUS, ps)
         ref_c, ref_m = oracle.opportunity(draft, y, regret, vocab, lens, TAUS, ps)
         assert m == ref_m and np.array_equal(counts, ref_c), p_match
-
-
-def test_opportunity_needs_offsets_above_1024_requests():
-    lens = np.zeros(1025, dtype=np.int32)
-    rows = 1025
-    z = np.zeros(rows, dtype=np.int32)
-    with pytest.raises(asd.AsdError):
-        gpu_counts(z, z, np.zeros(rows, np.float32), 10, lens, TAUS, PS)
 
 
 def test_opportunity_explicit_offsets_and_invalid_requests():
