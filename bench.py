@@ -245,6 +245,9 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="a step is every call of the workload with its commit "
                          "(asd_verify_commit), captured once as a HIP graph and replayed")
+    ap.add_argument("--caller-workspace", action="store_true",
+                    help="with --graph: asd_verify_commit with a caller workspace (the two-launch "
+                         "form) instead of the library workspace")
     ap.add_argument("--separate-commit", action="store_true",
                     help="with --graph: asd_verify_ws then asd_commit (two calls per round) "
                          "instead of asd_verify_commit")
@@ -305,8 +308,10 @@ def main():
     if args.graph:
         if args.shards or args.opportunity:
             raise SystemExit("--graph runs the plain verifier calls")
-        nbytes = asd.asd_workspace_bytes(logits.dtype, w.vocab, w.num_requests, n)
-        ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        ws = None                        # the library workspace: one launch per small call
+        if args.caller_workspace or args.separate_commit:
+            nbytes = asd.asd_workspace_bytes(logits.dtype, w.vocab, w.num_requests, n)
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         capacity = (args.warmup + args.steps + 2) * w.blocks * (int(w.block_lens.max()) + 1)
         tokens = torch.zeros((w.num_requests, capacity), dtype=torch.int32, device=dev)
         seq_len = torch.zeros(w.num_requests, dtype=torch.int64, device=dev)
@@ -324,6 +329,12 @@ def main():
         graph = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream(dev)
         side.wait_stream(torch.cuda.current_stream(dev))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):    # creates the stream's library workspace before capture
+            eager_step()
+        torch.cuda.synchronize()
+        budget.copy_(pristine)
+        seq_len.zero_()
         torch.cuda.synchronize()
         with torch.cuda.graph(graph, stream=side):
             eager_step()

@@ -111,6 +111,15 @@ typedef struct {
  *    a_i = 0, next token = -1, ledger untouched.
  *  Both cases also set a bit of the device error word (asd_device_error).
  *
+ * Small calls (at most 512 row tiles and 8 requests, the latency-bound
+ * regime of single-request decoding) that are not being captured run as one
+ * kernel launch instead of two: the last row tile to finish runs the scan.
+ * This form needs a zeroed counter, so it runs only with a library workspace
+ * (here, asd_verify_ex and asd_verify_commit without a workspace, and
+ * asd_verify_static); with a caller's workspace, or during stream capture
+ * (where launches are cheap and two kernels are faster), the two-launch form
+ * runs.  The results are the same.
+ *
  * Outputs must not alias the inputs.  Calls that share the library workspace
  * of one (device, stream) pair are ordered by the stream; calls on different
  * streams use different workspaces.  The first call on a (device, stream)
@@ -168,12 +177,14 @@ asd_status asd_verify_ws(const void *logits, asd_dtype dtype, int64_t vocab,
  * call's workspace is a fixed device array of ASD_STATIC_SCRATCH_BYTES bytes
  * that the library holds on every device it runs on until the process ends;
  * the call never calls hipMalloc or hipFree.  A call whose workspace
- * (asd_workspace_bytes) exceeds that size returns ASD_ESCRATCH with nothing
- * launched: it needs 8 bytes per request, 8 per row, and 16 per vocabulary
- * split of a row when rows are split (about 500,000 whole rows fit).
- * Every call on a device shares that device's array, which keeps the last
- * call's contents; nothing in it needs to start at zero or is carried from one
- * call to the next.  Calls that may overlap on one device (different streams,
+ * (asd_workspace_bytes) exceeds that size less 256 bytes returns ASD_ESCRATCH
+ * with nothing launched: it needs 8 bytes per request, 8 per row, and 16 per
+ * vocabulary split of a row when rows are split (about 500,000 whole rows
+ * fit).  Every call on a device shares that device's array, which keeps the
+ * last call's contents.  Its first 256 bytes hold the counter of the
+ * single-launch form, zero when the library is loaded and left zero by every
+ * call; nothing else in it needs to start at zero or is carried from one call
+ * to the next.  Calls that may overlap on one device (different streams,
  * or host threads without ordering) race on the array and must not be issued;
  * calls in order on one stream are safe.  The first call on a device looks up
  * the array's address.

@@ -129,12 +129,27 @@ asd_status check_args(const void* logits, asd_dtype dtype, int64_t vocab, int32_
     return ASD_OK;
 }
 
+// The counter of the single-launch form for a call on stream `s`, or nullptr
+// for the two-launch form.  Eager small calls are bound by host launches, so
+// one launch wins (workload 1, eager: 12.6 against 15.3 us per call); inside a
+// captured graph launches cost little and the two kernels are faster than one
+// whose last tile runs the scan after every tile's release (7.7 against 9.4
+// us per round), so a call being captured takes two launches.
+unsigned* single_launch_counter(hipStream_t s, unsigned* counter) {
+    if (counter == nullptr) return nullptr;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone)
+        return nullptr;
+    return counter;
+}
+
 asd_status enqueue(const void* logits, asd_dtype dtype, int64_t vocab, int32_t num_requests,
                    int64_t total_rows, const int32_t* draft_tokens, const int32_t* block_lens,
                    const int64_t* row_offsets, const float* tau, const int32_t* exc_cap,
                    asd_budget* budget, int32_t* out_accept_len, int32_t* out_next_token,
                    int32_t* out_argmax, float* out_regret, hipStream_t stream, const Plan& plan,
-                   void* workspace, int32_t* commit_tokens = nullptr, int64_t commit_capacity = 0,
+                   void* workspace, unsigned* counter, int32_t* commit_tokens = nullptr,
+                   int64_t commit_capacity = 0,
                    int64_t* commit_seq_len = nullptr, int32_t* commit_done = nullptr,
                    bool raw_gate = false) {
     CallArgs a;
@@ -158,7 +173,10 @@ asd_status enqueue(const void* logits, asd_dtype dtype, int64_t vocab, int32_t n
     (void)dtype;
     (void)vocab;
     (void)total_rows;
-    return launch_verify(plan, a, workspace, stream) == hipSuccess ? ASD_OK : ASD_EHIP;
+    return launch_verify(plan, a, workspace, single_launch_counter(stream, counter), stream) ==
+                   hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
 }
 
 asd_status plan_for(asd_dtype dtype, int64_t vocab, int32_t num_requests, int64_t total_rows,
@@ -179,8 +197,12 @@ asd_status plan_for(asd_dtype dtype, int64_t vocab, int32_t num_requests, int64_
 
 // The library-owned workspace of (current device, stream), grown to at least
 // `bytes` (and at least doubled, so the retired buffers total less than the
-// current one); growth (hipMalloc) is refused during stream capture.
-asd_status library_workspace(hipStream_t s, size_t bytes, void** out) {
+// current one); growth (hipMalloc) is refused during stream capture.  Every
+// buffer starts with a header that holds the counter of single-launch calls,
+// zeroed when the buffer is allocated (calls leave it zero); `out` is the
+// memory after it, `counter` (optional) the header.
+asd_status library_workspace(hipStream_t s, size_t bytes, void** out,
+                             unsigned** counter = nullptr) {
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return ASD_EHIP;
     std::lock_guard<std::mutex> lock(g_mutex);
@@ -193,25 +215,33 @@ asd_status library_workspace(hipStream_t s, size_t bytes, void** out) {
         if (want < 2 * w.bytes) want = 2 * w.bytes;
         want = align_up(want, (size_t)1 << 20);
         void* p = nullptr;
-        if (hipMalloc(&p, want) != hipSuccess) return ASD_ENOMEM;
+        if (hipMalloc(&p, want + kCounterHeaderBytes) != hipSuccess) return ASD_ENOMEM;
+        if (hipMemsetAsync(p, 0, kCounterHeaderBytes, s) != hipSuccess) {
+            (void)hipFree(p);
+            return ASD_EHIP;
+        }
         if (w.ptr) w.retired.push_back(w.ptr);
         w.ptr = p;
         w.bytes = want;
     }
-    *out = w.ptr;
+    *out = (unsigned char*)w.ptr + kCounterHeaderBytes;
+    if (counter) *counter = (unsigned*)w.ptr;
     return ASD_OK;
 }
 
 // The caller's workspace when given (size checked; its alignment is checked
 // with the other host arguments), else the library's.
+// A caller's workspace has any content, so it gets no counter (the two-kernel
+// form runs).
 asd_status resolve_workspace(hipStream_t s, const Plan& plan, void* workspace,
-                             size_t workspace_bytes, void** out) {
+                             size_t workspace_bytes, void** out, unsigned** counter) {
     if (workspace) {
         if (workspace_bytes < plan.ws_bytes) return ASD_ENOMEM;
         *out = workspace;
+        *counter = nullptr;
         return ASD_OK;
     }
-    return library_workspace(s, plan.ws_bytes, out);
+    return library_workspace(s, plan.ws_bytes, out, counter);
 }
 
 }  // namespace
@@ -236,10 +266,11 @@ asd_status asd_verify(const void* logits, asd_dtype dtype, int64_t vocab, int32_
 
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;
-    if ((st = library_workspace(s, plan.ws_bytes, &ws)) != ASD_OK) return st;
+    unsigned* counter = nullptr;
+    if ((st = library_workspace(s, plan.ws_bytes, &ws, &counter)) != ASD_OK) return st;
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
-                   out_argmax, out_regret, s, plan, ws);
+                   out_argmax, out_regret, s, plan, ws, counter);
 }
 
 size_t asd_workspace_bytes(asd_dtype dtype, int64_t vocab, int32_t num_requests,
@@ -270,7 +301,7 @@ asd_status asd_verify_ws(const void* logits, asd_dtype dtype, int64_t vocab,
     if (workspace_bytes < plan.ws_bytes) return ASD_ENOMEM;
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
-                   out_argmax, out_regret, (hipStream_t)stream, plan, workspace);
+                   out_argmax, out_regret, (hipStream_t)stream, plan, workspace, nullptr);
 }
 
 asd_status asd_verify_ex(const void* logits, asd_dtype dtype, int64_t vocab,
@@ -291,10 +322,12 @@ asd_status asd_verify_ex(const void* logits, asd_dtype dtype, int64_t vocab,
     if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;
-    if ((st = resolve_workspace(s, plan, workspace, workspace_bytes, &ws)) != ASD_OK) return st;
+    unsigned* counter = nullptr;
+    if ((st = resolve_workspace(s, plan, workspace, workspace_bytes, &ws, &counter)) != ASD_OK)
+        return st;
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
-                   out_argmax, out_regret, s, plan, ws, nullptr, 0, nullptr, nullptr,
+                   out_argmax, out_regret, s, plan, ws, counter, nullptr, 0, nullptr, nullptr,
                    (flags & ASD_GATE_RAW) != 0);
 }
 
@@ -311,12 +344,15 @@ asd_status asd_verify_static(const void* logits, asd_dtype dtype, int64_t vocab,
     if (st != ASD_OK || num_requests == 0) return st;
     Plan plan;
     if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
-    if (plan.ws_bytes > kStaticScratchBytes) return ASD_ESCRATCH;
-    void* ws = nullptr;
-    if (static_scratch_address(&ws) != hipSuccess) return ASD_EHIP;
+    if (plan.ws_bytes > kStaticScratchBytes - kCounterHeaderBytes) return ASD_ESCRATCH;
+    void* base = nullptr;
+    if (static_scratch_address(&base) != hipSuccess) return ASD_EHIP;
+    // the scratch starts with the single-launch counter (zero at load, left
+    // zero by every call), then the call's workspace
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
-                   out_argmax, out_regret, (hipStream_t)stream, plan, ws);
+                   out_argmax, out_regret, (hipStream_t)stream, plan,
+                   (unsigned char*)base + kCounterHeaderBytes, (unsigned*)base);
 }
 
 asd_status asd_device_error(uint32_t* out_word, int32_t clear, void* stream) {
@@ -472,10 +508,13 @@ asd_status asd_verify_commit(const void* logits, asd_dtype dtype, int64_t vocab,
     if ((st = plan_for(dtype, vocab, num_requests, total_rows, &plan)) != ASD_OK) return st;
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;
-    if ((st = resolve_workspace(s, plan, workspace, workspace_bytes, &ws)) != ASD_OK) return st;
+    unsigned* counter = nullptr;
+    if ((st = resolve_workspace(s, plan, workspace, workspace_bytes, &ws, &counter)) != ASD_OK)
+        return st;
     return enqueue(logits, dtype, vocab, num_requests, total_rows, draft_tokens, block_lens,
                    row_offsets, tau, exc_cap, budget_inout, out_accept_len, out_next_token,
-                   out_argmax, out_regret, s, plan, ws, tokens, capacity, seq_len, out_committed);
+                   out_argmax, out_regret, s, plan, ws, counter, tokens, capacity, seq_len,
+                   out_committed);
 }
 
 asd_status asd_lmhead_verify(const void* hidden, const void* weight, int64_t d, int64_t vocab,

@@ -599,24 +599,20 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
 
 // ----------------------------------------------------------- stage 1 kernel
 
-// `logits` rows hold columns [col_offset, col_offset + vocab) of the full
-// vocabulary (col_offset = 0 and vocab = V unless the rows are one tensor-
-// parallel shard); columns are reported globally.  With `partials` set every
-// tile writes a partial (split rows, or one shard of each row); otherwise each
-// row is one tile and writes its record.  Six wavefronts per SIMD: the two load
-// buffers fit in 80 VGPRs with no spill (a tighter budget spills).
+// One tile of the row pass, the body of the row kernels.  `logits` rows hold
+// columns [col_offset, col_offset + vocab) of the full vocabulary (col_offset
+// = 0 and vocab = V unless the rows are one tensor-parallel shard); columns are
+// reported globally.  With `partials` set the tile writes a partial (split
+// rows, or one shard of each row); otherwise the row is one tile and writes its
+// record.  Thread 0 writes; every thread returns.
 template <int EB>
-__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(6))) void asd_row_kernel(
+__device__ __forceinline__ void row_tile(
     const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
     int64_t chunk_vecs, const int32_t* __restrict__ draft_tokens,
     TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
-    int32_t* __restrict__ out_argmax, int32_t num_requests,
-    const int32_t* __restrict__ block_lens, int64_t* __restrict__ packed_offsets) {
+    int32_t* __restrict__ out_argmax) {
     constexpr int kEpv = 16 / EB;
     const int tid = threadIdx.x;
-    if (packed_offsets != nullptr && blockIdx.x == 0)
-        write_packed_offsets(num_requests, block_lens, packed_offsets);
-
     const int64_t row = blockIdx.x / splits;
     const int split = (int)(blockIdx.x - row * splits);
     const unsigned char* row_ptr = logits + row * vocab * EB;
@@ -661,7 +657,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(6))
     }
     if (tid != 0) return;
 
-    if (partials != nullptr) {           // combined by the scan kernel
+    if (partials != nullptr) {           // combined by the scan
         TilePartial tp;
         tp.packed = packed;
         tp.bits = bits;
@@ -682,6 +678,23 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(6))
     }
     records[row] = rec;
     if (out_argmax) out_argmax[row] = y;
+}
+
+// The row pass as its own kernel, followed by the scan kernel.  Block 0 also
+// writes the packed row offsets of the requests when `packed_offsets` is set.
+// Six wavefronts per SIMD: the two load buffers fit in 80 VGPRs with no spill
+// (a tighter budget spills).
+template <int EB>
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(6))) void asd_row_kernel(
+    const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
+    int64_t chunk_vecs, const int32_t* __restrict__ draft_tokens,
+    TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
+    int32_t* __restrict__ out_argmax, int32_t num_requests,
+    const int32_t* __restrict__ block_lens, int64_t* __restrict__ packed_offsets) {
+    if (packed_offsets != nullptr && blockIdx.x == 0)
+        write_packed_offsets(num_requests, block_lens, packed_offsets);
+    row_tile<EB>(logits, vocab, col_offset, splits, chunk_vecs, draft_tokens, partials, records,
+                 out_argmax);
 }
 
 // ----------------------------------------------------------- stage 2 kernel
@@ -766,41 +779,14 @@ __device__ __forceinline__ uint32_t lane_u32(uint32_t v, int lane) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
-__global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-
-    if ((int32_t)blockIdx.x >= A.request_blocks) {
-        // Argmax of every row when rows were split (one lane per row).
-        const int64_t row = (int64_t)(blockIdx.x - A.request_blocks) * kScanThreads + tid;
-        if (row < A.total_rows) {
-            unsigned long long packed;
-            uint32_t bits, draft_bits;
-            combine_row(A, row, -1, packed, bits, draft_bits);
-            A.out_argmax[row] = packed_col(packed);
-        }
-        return;
-    }
-
-    const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
-    if (i >= A.num_requests) return;
+// Algorithm 1 for request i, whose rows start at o, by one wavefront: lanes
+// are block positions.  Each lane forms its row's record (or combines the
+// row's partials); the wavefront walks the mismatches in position order.
+// Wave-uniform: every lane of the wavefront calls it with the same i and o.
+__device__ __forceinline__ void scan_request(const ScanArgs& A, int64_t i, int64_t o) {
+    const int lane = threadIdx.x & 63;
     const int32_t K_given = A.block_lens[i];
     const int32_t K = K_given > 0 ? K_given : 0;      // a negative K is read as 0
-    int64_t o;
-    if (A.offsets) {
-        o = A.offsets[i];
-    } else {
-        // Packed layout, few requests: this wavefront sums the row counts of
-        // the requests before it.
-        long long part = 0;
-#pragma unroll 4
-        for (int64_t j = lane; j < i; j += 64) {
-            const int32_t Kj = A.block_lens[j];
-            part += (long long)(Kj > 0 ? Kj : 0) + 1;
-        }
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
-        o = part;
-    }
     const int64_t L = A.commit_tokens ? A.commit_seq_len[i] : 0;   // loaded early
     if (K_given < 0 && lane == 0) atomicOr(&asd_error_word, kErrNegativeK);
     if (!(o >= 0 && o + (int64_t)K < A.total_rows)) {
@@ -905,6 +891,92 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
             if (!ok) atomicOr(&asd_error_word, kErrCommit);
         }
     }
+}
+
+__global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+    if ((int32_t)blockIdx.x >= A.request_blocks) {
+        // Argmax of every row when rows were split (one lane per row).
+        const int64_t row = (int64_t)(blockIdx.x - A.request_blocks) * kScanThreads + tid;
+        if (row < A.total_rows) {
+            unsigned long long packed;
+            uint32_t bits, draft_bits;
+            combine_row(A, row, -1, packed, bits, draft_bits);
+            A.out_argmax[row] = packed_col(packed);
+        }
+        return;
+    }
+
+    const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
+    if (i >= A.num_requests) return;
+    int64_t o;
+    if (A.offsets) {
+        o = A.offsets[i];
+    } else {
+        // Packed layout, few requests: this wavefront sums the row counts of
+        // the requests before it.
+        long long part = 0;
+#pragma unroll 4
+        for (int64_t j = lane; j < i; j += 64) {
+            const int32_t Kj = A.block_lens[j];
+            part += (long long)(Kj > 0 ? Kj : 0) + 1;
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
+        o = part;
+    }
+    scan_request(A, i, o);
+}
+
+// ---------------------------------------------- single-launch verification
+//
+// For plans with few tiles and few requests the call is bound by latency, and
+// the second launch of the scan is a large share of it.  Here the row pass and
+// the scan run in one launch: every tile counts itself done on a counter, with
+// release order after its record or partial, and the one tile that finds
+// itself last (acquire order) runs Algorithm 1 for every request, one
+// wavefront per request, writes the argmax of split rows and resets the
+// counter to zero for the next call.  No tile waits for another.  The counter
+// must be zero when the call starts: it lives in a header of the library's
+// workspaces that is zeroed when they are allocated, and every call leaves it
+// at zero.
+// Small plans have at most two tiles per CU, so the kernel takes the registers
+// it needs (no occupancy bound).
+template <int EB>
+__global__ __launch_bounds__(kRowThreads) void asd_row_scan_kernel(const unsigned char* __restrict__ logits, int64_t vocab, int splits,
+                    int64_t chunk_vecs, TilePartial* __restrict__ partials,
+                    RowRecord* __restrict__ records, unsigned* __restrict__ counter,
+                    const ScanArgs A) {
+    row_tile<EB>(logits, vocab, 0, splits, chunk_vecs, A.draft_tokens, partials, records,
+                 splits == 1 ? A.out_argmax : nullptr);
+    __shared__ int s_last;
+    if (threadIdx.x == 0) {
+        const unsigned prev =
+            __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = prev == gridDim.x - 1;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // every tile's output, for every thread
+
+    __shared__ int64_t s_off[kRowThreads];
+    for (int64_t first = 0; first < A.num_requests; first += kRowThreads) {
+        const int count = (int)min((int64_t)kRowThreads, (int64_t)A.num_requests - first);
+        block_offsets(A.num_requests, A.block_lens, A.offsets, first, count, s_off);
+        for (int k = threadIdx.x >> 6; k < count; k += kWaves)   // wave-uniform
+            scan_request(A, first + k, s_off[k]);
+        __syncthreads();
+    }
+    if (splits > 1 && A.out_argmax) {
+        for (int64_t row = threadIdx.x; row < A.total_rows; row += kRowThreads) {
+            unsigned long long packed;
+            uint32_t bits, draft_bits;
+            combine_row(A, row, -1, packed, bits, draft_bits);
+            A.out_argmax[row] = packed_col(packed);
+        }
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Packed row offsets for the calls that have no row kernel before the scan.
@@ -1430,10 +1502,31 @@ asd_read_probe_kernel(const unsigned char* __restrict__ buf, int64_t row_bytes,
 // ------------------------------------------------------------------ launch
 
 hipError_t launch_verify(const Plan& plan, const CallArgs& a, void* workspace,
-                         hipStream_t stream) {
+                         unsigned* counter, hipStream_t stream) {
     unsigned char* ws = (unsigned char*)workspace;
     RowRecord* records = (RowRecord*)(ws + plan.off_records);
     TilePartial* partials = plan.splits > 1 ? (TilePartial*)(ws + plan.off_partials) : nullptr;
+
+    if (counter != nullptr && single_launch(plan)) {
+        ScanArgs A = scan_args(a, plan.rows, plan.vocab, plan.elem_bytes);
+        A.splits = plan.splits;
+        A.chunk_vecs = plan.chunk_vecs;
+        A.offsets = a.row_offsets;                      // NULL: packed, formed in LDS
+        A.records = plan.splits == 1 ? records : nullptr;
+        A.partials = partials;
+        A.shard_vocab = 0;
+        const dim3 grid((unsigned)(plan.rows * plan.splits));
+        if (plan.elem_bytes == 2)
+            asd_row_scan_kernel<2><<<grid, kRowThreads, 0, stream>>>(
+                (const unsigned char*)a.logits, plan.vocab, plan.splits, plan.chunk_vecs, partials,
+                records, counter, A);
+        else
+            asd_row_scan_kernel<4><<<grid, kRowThreads, 0, stream>>>(
+                (const unsigned char*)a.logits, plan.vocab, plan.splits, plan.chunk_vecs, partials,
+                records, counter, A);
+        return hipGetLastError();
+    }
+
     int64_t* packed = a.row_offsets ? nullptr : (int64_t*)(ws + plan.off_offsets);
 
     const dim3 grid((unsigned)(plan.rows * plan.splits));

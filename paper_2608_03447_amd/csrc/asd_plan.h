@@ -94,8 +94,24 @@ struct CallArgs {
 Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int32_t num_requests,
                int num_cus);
 
+// Plans small enough for one launch (row pass and scan in one kernel; see
+// asd_row_scan_kernel): few tiles, and few requests, since the last tile scans
+// every request with its four wavefronts.
+constexpr int64_t kSingleLaunchMaxTiles = 512;
+constexpr int32_t kSingleLaunchMaxRequests = 8;
+inline bool single_launch(const Plan& p) {
+    return p.rows * p.splits <= kSingleLaunchMaxTiles &&
+           p.num_requests <= kSingleLaunchMaxRequests;
+}
+
+// Bytes of the header in front of every library-owned workspace (and of the
+// fixed scratch): the counter of single-launch calls, zero between calls.
+constexpr size_t kCounterHeaderBytes = 256;
+
+// `counter`: a zero counter the call may use for the single-launch form (it
+// leaves it zero), or nullptr for the two-kernel form.
 hipError_t launch_verify(const Plan& plan, const CallArgs& args, void* workspace,
-                         hipStream_t stream);
+                         unsigned* counter, hipStream_t stream);
 
 // One vocabulary shard: rows of `shard_vocab` columns that are columns
 // [vocab_offset, vocab_offset + shard_vocab) of the full vocabulary.  Writes one

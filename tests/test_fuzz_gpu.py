@@ -19,10 +19,11 @@ SPECIAL_F32 = np.array([0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC000
                        dtype=np.uint32)
 
 
-def _case(rng, large_vocab=False):
+def _case(rng, large_vocab=False, max_requests=None):
     """One random call.  With `large_vocab` the vocabulary is 8,191 to 151,936
     entries and there are at most six requests, so rows are split over several
-    workgroups (a split plan); otherwise V <= 5,003 and rows are whole."""
+    workgroups (a split plan); otherwise V <= 5,003 and rows are whole.
+    `max_requests` bounds the number of requests further."""
     dtype = "bf16" if rng.random() < 0.6 else "f32"
     if large_vocab:
         vocab = int(rng.choice([8191, 16385, 32000, 50257, 129280, 151936]))
@@ -30,6 +31,8 @@ def _case(rng, large_vocab=False):
     else:
         vocab = int(rng.choice([1, 2, 7, 64, 257, 1000, 1031, 4096, 5003]))
         n = int(rng.integers(1, 40))
+    if max_requests is not None:
+        n = min(n, int(rng.integers(1, max_requests + 1)))
     lens = rng.integers(-2, 20, n).astype(np.int32)
     offsets = None
     rows = int(np.sum(np.maximum(lens, 0) + 1))
@@ -79,9 +82,13 @@ def test_random_split_plan_calls_match_the_oracle(block):
     _run_block(np.random.default_rng(7000 + block), "fuzz-split %d" % block, large_vocab=True)
 
 
-def _run_block(rng, name, large_vocab):
-    for case in range(25):
-        dtype, logits, draft, lens, offsets, tau, cap, budget, raw_gate = _case(rng, large_vocab)
+def _run_block(rng, name, large_vocab, max_requests=None, caller_workspace=False, cases=25):
+    """`cases` random calls against the oracle.  With `caller_workspace` every
+    call gets a workspace of its own (so the two-launch form runs); otherwise
+    the library's, where small calls run as one launch."""
+    for case in range(cases):
+        dtype, logits, draft, lens, offsets, tau, cap, budget, raw_gate = _case(
+            rng, large_vocab, max_requests)
         rows, vocab = logits.shape
         n = len(lens)
         label = "%s.%d: %s rows %d vocab %d requests %d offsets %s raw_gate %s" % (
@@ -102,16 +109,21 @@ def _run_block(rng, name, large_vocab):
         torch.cuda.synchronize()
         asd.asd_device_error(clear=True)
         use_commit = (not raw_gate) and rng.random() < 0.5
+        ws = None
+        if caller_workspace:
+            ws = torch.full((asd.asd_workspace_bytes(tl.dtype, vocab, n, rows),), 0xA5,
+                            dtype=torch.uint8, device=DEV)
         if use_commit:
             tok, sl = t(tokens0.copy()), t(start.copy())
             done = torch.empty(n, dtype=torch.int32, device=DEV)
             acc, nxt = asd.asd_verify_commit(tl, t(draft), t(lens), t(tau), t(cap), tb, tok, sl,
                                              row_offsets=to, out_argmax=amax, out_regret=regret,
-                                             out_committed=done)
+                                             out_committed=done, workspace=ws)
         else:
             acc, nxt = asd.asd_verify_ex(tl, t(draft), t(lens), t(tau), t(cap), tb,
                                          flags=asd.ASD_GATE_RAW if raw_gate else 0,
-                                         row_offsets=to, out_argmax=amax, out_regret=regret)
+                                         workspace=ws, row_offsets=to, out_argmax=amax,
+                                         out_regret=regret)
         torch.cuda.synchronize()
         word = asd.asd_device_error(clear=True)
         g = {"accept_len": acc.cpu().numpy(), "next_token": nxt.cpu().numpy(),
