@@ -783,11 +783,33 @@ __device__ __forceinline__ uint32_t lane_u32(uint32_t v, int lane) {
 // are block positions.  Each lane forms its row's record (or combines the
 // row's partials); the wavefront walks the mismatches in position order.
 // Wave-uniform: every lane of the wavefront calls it with the same i and o.
-__device__ __forceinline__ void scan_request(const ScanArgs& A, int64_t i, int64_t o) {
+// The per-request inputs of Algorithm 1 (block length, ledger, gate, cap and
+// committed length), loaded together so that their loads are in flight at
+// once, ahead of the rows.
+struct RequestIn {
+    int32_t K_given;
+    int32_t M;
+    float2 ledger;
+    float g;
+    int64_t L;
+};
+
+__device__ __forceinline__ RequestIn load_request(const ScanArgs& A, int64_t i) {
+    RequestIn q;
+    q.K_given = A.block_lens[i];
+    q.ledger = A.budget[i];
+    q.g = A.tau[i];
+    q.M = A.exc_cap[i];
+    q.L = A.commit_tokens ? A.commit_seq_len[i] : 0;
+    return q;
+}
+
+__device__ __forceinline__ void scan_request(const ScanArgs& A, int64_t i, int64_t o,
+                                             const RequestIn& q) {
     const int lane = threadIdx.x & 63;
-    const int32_t K_given = A.block_lens[i];
+    const int32_t K_given = q.K_given;
     const int32_t K = K_given > 0 ? K_given : 0;      // a negative K is read as 0
-    const int64_t L = A.commit_tokens ? A.commit_seq_len[i] : 0;   // loaded early
+    const int64_t L = q.L;
     if (K_given < 0 && lane == 0) atomicOr(&asd_error_word, kErrNegativeK);
     if (!(o >= 0 && o + (int64_t)K < A.total_rows)) {
         if (lane == 0) {
@@ -798,11 +820,10 @@ __device__ __forceinline__ void scan_request(const ScanArgs& A, int64_t i, int64
         }
         return;
     }
-    const float2 ledger = A.budget[i];
-    const float B = ledger.x;
-    const float s = ledger.y;
-    const float g = A.tau[i];
-    const int32_t M = A.exc_cap[i];
+    const float B = q.ledger.x;
+    const float s = q.ledger.y;
+    const float g = q.g;
+    const int32_t M = q.M;
     const bool strict = (B == 0.0f);   // Algorithm 1: B = 0 -> exact greedy verification
 
     int32_t a = 0, N = 0, next = -1;
@@ -910,6 +931,7 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
 
     const int64_t i = (int64_t)blockIdx.x * (kScanThreads / 64) + wave;   // wave-uniform
     if (i >= A.num_requests) return;
+    const RequestIn q = load_request(A, i);
     int64_t o;
     if (A.offsets) {
         o = A.offsets[i];
@@ -926,7 +948,7 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
         for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
         o = part;
     }
-    scan_request(A, i, o);
+    scan_request(A, i, o, q);
 }
 
 // ---------------------------------------------- single-launch verification
@@ -943,11 +965,38 @@ __global__ __launch_bounds__(kScanThreads) void asd_scan_kernel(const ScanArgs A
 // at zero.
 // Small plans have at most two tiles per CU, so the kernel takes the registers
 // it needs (no occupancy bound).
+static_assert(kSingleLaunchMaxRequests <= 2 * kWaves, "two requests per wavefront at most");
+
 template <int EB>
 __global__ __launch_bounds__(kRowThreads) void asd_row_scan_kernel(const unsigned char* __restrict__ logits, int64_t vocab, int splits,
                     int64_t chunk_vecs, TilePartial* __restrict__ partials,
                     RowRecord* __restrict__ records, unsigned* __restrict__ counter,
                     const ScanArgs A) {
+    // The requests' inputs and row offsets are loaded before the row pass (the
+    // few requests of a single-launch plan: wavefront w takes requests w and
+    // w + 4), so that the last tile's scan waits only for the rows.
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    RequestIn q[2];
+    int64_t o[2];
+    {
+        const int n = A.num_requests;            // <= kSingleLaunchMaxRequests <= 64
+        const int32_t Kl = lane < n ? A.block_lens[lane] : 0;
+        long long incl = lane < n ? (long long)(Kl > 0 ? Kl : 0) + 1 : 0;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const long long t = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += t;
+        }
+        const long long excl = incl - (lane < n ? (long long)(Kl > 0 ? Kl : 0) + 1 : 0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int k = wave + 4 * j;
+            if (k < n) {
+                q[j] = load_request(A, k);
+                o[j] = A.offsets ? A.offsets[k] : (int64_t)__shfl(excl, k, 64);
+            }
+        }
+    }
     row_tile<EB>(logits, vocab, 0, splits, chunk_vecs, A.draft_tokens, partials, records,
                  splits == 1 ? A.out_argmax : nullptr);
     __shared__ int s_last;
@@ -960,14 +1009,9 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_scan_kernel(const unsigne
     if (!s_last) return;
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // every tile's output, for every thread
 
-    __shared__ int64_t s_off[kRowThreads];
-    for (int64_t first = 0; first < A.num_requests; first += kRowThreads) {
-        const int count = (int)min((int64_t)kRowThreads, (int64_t)A.num_requests - first);
-        block_offsets(A.num_requests, A.block_lens, A.offsets, first, count, s_off);
-        for (int k = threadIdx.x >> 6; k < count; k += kWaves)   // wave-uniform
-            scan_request(A, first + k, s_off[k]);
-        __syncthreads();
-    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+        if (wave + 4 * j < A.num_requests) scan_request(A, wave + 4 * j, o[j], q[j]);
     if (splits > 1 && A.out_argmax) {
         for (int64_t row = threadIdx.x; row < A.total_rows; row += kRowThreads) {
             unsigned long long packed;

@@ -98,7 +98,7 @@ Plan make_plan(int elem_bytes, int64_t vocab, int64_t rows, int32_t num_requests
 // asd_row_scan_kernel): few tiles, and few requests, since the last tile scans
 // every request with its four wavefronts.
 constexpr int64_t kSingleLaunchMaxTiles = 512;
-constexpr int32_t kSingleLaunchMaxRequests = 8;
+constexpr int32_t kSingleLaunchMaxRequests = 8;   // two per wavefront of the last tile
 inline bool single_launch(const Plan& p) {
     return p.rows * p.splits <= kSingleLaunchMaxTiles &&
            p.num_requests <= kSingleLaunchMaxRequests;
