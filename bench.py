@@ -750,18 +750,29 @@ def bench_lmhead(args, torch, asd, W):
     def gemm_only():
         torch.nn.functional.linear(hidden, weight, out=logits)
 
+    # The practical matrix-core ceiling of this launch: the kernel's MFMA work
+    # over as many workgroups and K steps, with operands of the same
+    # distribution held in registers (asd_mfma_probe), no memory traffic.
+    tiles = ((rows + 255) // 256) * ((V + 255) // 256)
+    probe_out = torch.empty(tiles, dtype=torch.int32, device=dev)
+
+    def mfma_probe():
+        asd.asd_mfma_probe(hidden, tiles, d // 64, probe_out)
+
     # Alternate the three paths over rounds so clock and thermal drift affect
     # them alike; report the median of each.
     fused()
     torch.cuda.synchronize()
-    f_ms, u_ms, g_ms = [], [], []
+    f_ms, u_ms, g_ms, p_ms = [], [], [], []
     for _ in range(3):
         f_ms.append(timed(fused))
         u_ms.append(timed(unfused))
         g_ms.append(timed(gemm_only))
-    fused_ms, unfused_ms, gemm_ms = (sorted(v)[1] for v in (f_ms, u_ms, g_ms))
+        p_ms.append(timed(mfma_probe))
+    fused_ms, unfused_ms, gemm_ms, probe_ms = (sorted(v)[1] for v in (f_ms, u_ms, g_ms, p_ms))
     log("fused %.3f ms, unfused (library GEMM + logits + asd_verify) %.3f ms, library GEMM alone "
-        "%.3f ms (medians of 3 alternating rounds)" % (fused_ms, unfused_ms, gemm_ms))
+        "%.3f ms, matrix-core probe %.3f ms (medians of 3 alternating rounds)" % (
+            fused_ms, unfused_ms, gemm_ms, probe_ms))
 
     # Check a sample of rows against exact logits on the host: the argmax must
     # agree wherever the top-two gap exceeds the rounding bound.
@@ -798,6 +809,14 @@ def bench_lmhead(args, torch, asd, W):
                      "traffic": lm_traffic,
                      "traffic_source": traffic_note(lm_tag, "asd_lmhead_kernel")
                      if lm_traffic else None},
+        "practical_mfma": {
+            "kernel": "asd_mfma_probe (the LM-head kernel's MFMA work on register operands of the "
+                      "same distribution, no memory traffic)",
+            "workgroups": tiles, "steps": d // 64, "avg_launch_ms": probe_ms,
+            "achieved": tiles * (d // 64) * 2.0 ** 23 / (probe_ms / 1e3) / 1e12,
+            "unit": "TFLOP/s",
+            "frac": tiles * (d // 64) * 2.0 ** 23 / (probe_ms / 1e3) / 1e12 / 2500.0,
+            "fused_call_time_over_probe": fused_ms / probe_ms},
         "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(out), flush=True)

@@ -435,6 +435,31 @@ asd_status asd_lmhead_verify(const void *hidden, const void *weight, int64_t d, 
 asd_status asd_read_probe(const void *buf, int64_t rows, int64_t row_bytes, uint32_t *out_word,
                           void *stream);
 
+/*
+ * asd_mfma_probe -- a measurement helper: the matrix-core work of
+ * asd_lmhead_verify with no memory traffic.  Each of `workgroups` workgroups
+ * has the LM-head kernel's shape (eight wavefronts, each with 4 x 2 tiles of
+ * 32 x 32 binary32 accumulators) and runs `steps` K steps of 64, i.e. 32
+ * v_mfma_f32_32x32x16_bf16 per wavefront per step (2^23 flops per workgroup
+ * per step), on operand fragments read once from `operands` and held in
+ * registers.  The matrix cores' power depends on their operands, so the caller
+ * passes data of the distribution it measures.  Run over an LM-head launch's
+ * workgroups and steps (steps = d / 64), its duration is the practical
+ * matrix-core ceiling of that launch under the chip's power limit.
+ *
+ * operands        device bf16 values, 16-byte aligned, `vectors` 16-byte
+ *                 vectors (>= 6); thread t of workgroup w reads the 6 vectors
+ *                 starting at ((w mod 64) * 512 + t) * 6, modulo `vectors`,
+ *                 and forms four fragment sets from them.
+ * workgroups      1 <= workgroups < 2^31;  steps >= 1.
+ * out             device uint32 [workgroups]: the binary32 bits of the sum of
+ *                 the accumulators of each workgroup's thread 0 (with every
+ *                 operand 1.0 this is 8192 * steps).
+ * Allocates nothing; asynchronous on `stream`.
+ */
+asd_status asd_mfma_probe(const void *operands, int64_t vectors, int64_t workgroups,
+                          int64_t steps, uint32_t *out, void *stream);
+
 /* Human-readable name of a status code (static storage). */
 const char *asd_status_string(asd_status status);
 

@@ -15,7 +15,7 @@ from .build import HASHED_SOURCES, LIBRARY, source_hash
 
 __all__ = ["asd_verify", "asd_verify_static", "asd_verify_ws", "asd_verify_ex", "asd_shard_argmax",
            "asd_verify_partials", "asd_opportunity", "asd_commit", "asd_verify_commit",
-           "asd_lmhead_verify", "asd_device_error", "asd_read_probe", "asd_workspace_bytes",
+           "asd_lmhead_verify", "asd_device_error", "asd_read_probe", "asd_mfma_probe", "asd_workspace_bytes",
            "asd_status_string", "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16",
            "ASD_GATE_RAW", "ASD_DEVERR_NEGATIVE_K", "ASD_DEVERR_ROWS", "ASD_DEVERR_COMMIT",
            "library_path", "library_source_hash", "check_built_from_sources"]
@@ -82,6 +82,8 @@ def _load():
     lib.asd_verify_ex.restype = ctypes.c_int
     lib.asd_device_error.argtypes = [vp, i32, vp]
     lib.asd_device_error.restype = ctypes.c_int
+    lib.asd_mfma_probe.argtypes = [vp, i64, i64, i64, vp, vp]
+    lib.asd_mfma_probe.restype = ctypes.c_int
     lib.asd_read_probe.argtypes = [vp, i64, i64, vp, vp]
     lib.asd_read_probe.restype = ctypes.c_int
     lib.asd_shard_argmax.argtypes = [vp, ctypes.c_int, i64, i64, i64, i64, vp, vp, vp]
@@ -314,6 +316,24 @@ def asd_read_probe(buf, rows, row_bytes, out_word):
                                     ctypes.c_void_p(out_word.data_ptr()), ctypes.c_void_p(stream))
     if st != 0:
         raise AsdError(st, "asd_read_probe")
+
+
+def asd_mfma_probe(operands, workgroups, steps, out):
+    """The LM-head kernel's matrix-core work without memory traffic
+    (``asd_mfma_probe``): ``operands`` a contiguous bfloat16 GPU tensor of at
+    least 48 values, ``out`` an int32 tensor of ``workgroups`` entries on the
+    same device (binary32 bits of each workgroup's thread-0 accumulator sum)."""
+    if operands.dtype != torch.bfloat16 or not operands.is_cuda or not operands.is_contiguous():
+        raise ValueError("operands must be a contiguous bfloat16 GPU tensor")
+    if out.dtype != torch.int32 or out.numel() < workgroups or out.device != operands.device:
+        raise ValueError("out must be an int32 tensor of at least `workgroups` entries")
+    with torch.cuda.device(operands.device):
+        stream = torch.cuda.current_stream(operands.device).cuda_stream
+        st = _load().asd_mfma_probe(ctypes.c_void_p(operands.data_ptr()), operands.numel() // 8,
+                                    int(workgroups), int(steps), ctypes.c_void_p(out.data_ptr()),
+                                    ctypes.c_void_p(stream))
+    if st != 0:
+        raise AsdError(st, "asd_mfma_probe")
 
 
 def asd_shard_argmax(shard_logits, vocab_offset, vocab, draft_tokens, out_partials=None):

@@ -21,7 +21,7 @@ namespace {
 size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
 
 // Tiles the row kernel aims for: at least two rounds of the resident 256-thread
-// workgroups per CU (six at the kernel's register budget), so that the last
+// workgroups per CU (five at the kernel's register budget), so that the last
 // round's stragglers are a small share of the stream (measured on MI355X: 4,352 whole rows of 297 KB
 // stream best unsplit; 2,112 rows of 607 KB gain 5% from two splits).
 constexpr int kTilesPerCu = 16;
@@ -553,6 +553,17 @@ asd_status asd_lmhead_verify(const void* hidden, const void* weight, int64_t d, 
     a.out_argmax = out_argmax;
     a.out_regret = out_regret;
     return launch_lmhead_verify(hidden, weight, d, vocab, total_rows, a, ws, s) == hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
+asd_status asd_mfma_probe(const void* operands, int64_t vectors, int64_t workgroups,
+                          int64_t steps, uint32_t* out, void* stream) {
+    if (!operands || !out || ((uintptr_t)operands & 15) != 0) return ASD_EINVAL;
+    if (vectors < 6 || workgroups < 1 || workgroups >= ((int64_t)1 << 31) || steps < 1)
+        return ASD_EINVAL;
+    return launch_mfma_probe(operands, vectors, workgroups, steps, out, (hipStream_t)stream) ==
+                   hipSuccess
                ? ASD_OK
                : ASD_EHIP;
 }

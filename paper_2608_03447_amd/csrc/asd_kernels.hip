@@ -162,13 +162,11 @@ __device__ __forceinline__ uint32_t dword_keys(uint32_t w) {
     }
 }
 
-// Max key over the 16-byte vectors of one group; vectors u >= nvalid are
-// ignored.  With raw and sign-magnitude keys `umax` also takes the greatest
-// pattern read as unsigned (per 16-bit half for bf16); masked vectors hold zero
-// and leave it.
-template <int EB, int kMode, bool kMasked>
-__device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], int nvalid,
-                                                 uint32_t& umax) {
+// Max key over the 16-byte vectors of one group.  With raw and sign-magnitude
+// keys `umax` also takes the greatest pattern read as unsigned (per 16-bit half
+// for bf16).
+template <int EB, int kMode>
+__device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], uint32_t& umax) {
     if constexpr (EB == 2) {
         uint32_t acc = KeyTraits<2>::kNonePacked;
 #pragma unroll
@@ -176,7 +174,6 @@ __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], in
             const uint32_t k0 = dword_keys<2, kMode>(raw[u].x), k1 = dword_keys<2, kMode>(raw[u].y);
             const uint32_t k2 = dword_keys<2, kMode>(raw[u].z), k3 = dword_keys<2, kMode>(raw[u].w);
             uint32_t m = pkmax16(pkmax16(k0, k1), pkmax16(k2, k3));
-            if (kMasked && u >= nvalid) m = KeyTraits<2>::kNonePacked;
             acc = pkmax16(acc, m);
             if constexpr (kMode != kKeysNan)
                 umax = pkmaxu16(umax, pkmaxu16(pkmaxu16(raw[u].x, raw[u].y),
@@ -193,7 +190,6 @@ __device__ __forceinline__ int32_t group_max_key(const u32x4 (&raw)[kUnroll], in
                                 (int32_t)dword_keys<4, kMode>(raw[u].y)),
                             max((int32_t)dword_keys<4, kMode>(raw[u].z),
                                 (int32_t)dword_keys<4, kMode>(raw[u].w)));
-            if (kMasked && u >= nvalid) m = KeyTraits<4>::kNone;
             acc = max(acc, m);
             if constexpr (kMode != kKeysNan)
                 umax = max(umax, max(max(raw[u].x, raw[u].y), max(raw[u].z, raw[u].w)));
@@ -377,17 +373,28 @@ __device__ void block_offsets(int32_t num_requests, const int32_t* __restrict__ 
 }
 
 // Where one lane's share of a tile lies: 16-byte vectors [v0, v1) of the row's
-// aligned middle, nfull whole groups of kGroupVecs vectors, then a partial one.
+// aligned middle, in ngroups groups of kGroupVecs vectors (the last one padded
+// with copies, see load_group).
 struct TileSpan {
     const u32x4* vec;
-    int32_t v0, v1, nv, nfull;    // vector counts: a row has fewer than 2^28 vectors
+    int32_t v0, v1, nv, ngroups;  // vector counts: a row has fewer than 2^28 vectors
     int tid;
 };
 
+// Group g of the lane's share.  In the tile's last group a vector past the
+// tile's end is read as a copy of the tile's last vector: a copy adds no new
+// value, and its column (past the end) is greater than the original's, so the
+// tile's first greatest element is unchanged.  Every group is then whole, and
+// the last one is loaded in the pipeline like the others.
 __device__ __forceinline__ void load_group(const TileSpan& t, u32x4 (&r)[kUnroll], int32_t g) {
-    const u32x4* p = t.vec + t.v0 + g * kGroupVecs + t.tid;
+    const int32_t i0 = t.v0 + g * kGroupVecs + t.tid;
+    const unsigned char* base = (const unsigned char*)t.vec;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(p + u * kRowThreads);
+    for (int u = 0; u < kUnroll; ++u) {
+        // a 32-bit byte offset from the row (a row is under 2^32 bytes)
+        const uint32_t off = (uint32_t)min(i0 + u * kRowThreads, t.v1 - 1) << 4;
+        r[u] = __builtin_nontemporal_load((const u32x4*)(base + off));
+    }
 }
 
 // The lane's first element holding `key` in a saved group, narrowed level by
@@ -395,8 +402,8 @@ __device__ __forceinline__ void load_group(const TileSpan& t, u32x4 (&r)[kUnroll
 // that vector's first such dword, then (bf16) the half.  Returns the element's
 // index within the group's vectors' elements and its binary32 bits.
 template <int EB, int kMode>
-__device__ __forceinline__ void find_first(const u32x4 (&saved)[kUnroll], int nvalid, int32_t key,
-                                           int& su, int& e, uint32_t& bits) {
+__device__ __forceinline__ void find_first(const u32x4 (&saved)[kUnroll], int32_t key, int& su,
+                                           int& e, uint32_t& bits) {
     su = 0;
     u32x4 sv = saved[0];
     bool hit = false;
@@ -406,7 +413,7 @@ __device__ __forceinline__ void find_first(const u32x4 (&saved)[kUnroll], int nv
                                    dword_max_key<EB, kMode>(saved[u].y)),
                                max(dword_max_key<EB, kMode>(saved[u].z),
                                    dword_max_key<EB, kMode>(saved[u].w)));
-        const bool take = !hit && u < nvalid && mk == key;
+        const bool take = !hit && mk == key;
         su = take ? u : su;
         sv = take ? saved[u] : sv;
         hit = hit || take;
@@ -455,16 +462,16 @@ __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t 
     auto rank_group = [&](const u32x4 (&r)[kUnroll], int32_t g) {
         int32_t gk;
         if (mode == kKeysNan) {
-            gk = group_max_key<EB, kKeysNan, false>(r, kUnroll, umax);
+            gk = group_max_key<EB, kKeysNan>(r, umax);
         } else if (mode == kKeysExact) {
-            gk = group_max_key<EB, kKeysExact, false>(r, kUnroll, umax);
+            gk = group_max_key<EB, kKeysExact>(r, umax);
         } else {
-            gk = group_max_key<EB, kKeysRaw, false>(r, kUnroll, umax);
+            gk = group_max_key<EB, kKeysRaw>(r, umax);
             if (mode == kKeysChoose) {
                 const int raw_ok =
                     __ballot(gk >= kRawExactFrom && gk <= KeyTraits<EB>::kInf) != 0ull;
                 mode = __builtin_amdgcn_readfirstlane(raw_ok) ? kKeysRaw : kKeysExact;
-                if (mode == kKeysExact) gk = group_max_key<EB, kKeysExact, false>(r, kUnroll, umax);
+                if (mode == kKeysExact) gk = group_max_key<EB, kKeysExact>(r, umax);
             }
         }
         const bool better = gk > best_key;
@@ -478,11 +485,11 @@ __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t 
     // keeps eight 16-byte loads per lane in flight while it computes.  The
     // scheduling barriers keep the compiler from moving ranking work (and its
     // waits) ahead of the loads.
-    if (t.nfull > 0) {
+    if (t.ngroups > 0) {
         u32x4 ra[kUnroll], rb[kUnroll];
         load_group(t, ra, 0);
         int32_t g = 0;
-        for (; g + 2 < t.nfull; g += 2) {
+        for (; g + 2 < t.ngroups; g += 2) {
             load_group(t, rb, g + 1);
             __builtin_amdgcn_sched_barrier(0);
             rank_group(ra, g);
@@ -490,7 +497,7 @@ __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t 
             __builtin_amdgcn_sched_barrier(0);
             rank_group(rb, g + 1);
         }
-        if (g + 1 < t.nfull) {
+        if (g + 1 < t.ngroups) {
             load_group(t, rb, g + 1);
             __builtin_amdgcn_sched_barrier(0);
             rank_group(ra, g);
@@ -499,42 +506,16 @@ __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t 
             rank_group(ra, g);
         }
     }
-    if (mode == kKeysChoose) mode = kKeysExact;      // no whole group: sign-magnitude keys
-    int best_nvalid = best_group >= 0 ? kUnroll : 0;
-
-    if (t.nv > t.nfull * kGroupVecs) {     // the tile's last, partial group
-        const int32_t first = t.v0 + t.nfull * kGroupVecs + t.tid;
-        int nvalid = 0;
-        u32x4 raw[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            raw[u] = (u32x4)(0u);
-            if (first + u * kRowThreads < t.v1) {
-                raw[u] = __builtin_nontemporal_load(t.vec + first + u * kRowThreads);
-                ++nvalid;
-            }
-        }
-        int32_t gk;
-        if (mode == kKeysRaw) gk = group_max_key<EB, kKeysRaw, true>(raw, nvalid, umax);
-        else if (mode == kKeysExact) gk = group_max_key<EB, kKeysExact, true>(raw, nvalid, umax);
-        else gk = group_max_key<EB, kKeysNan, true>(raw, nvalid, umax);
-        if (nvalid > 0 && gk > best_key) {
-            best_key = gk;
-            best_group = t.nfull;
-            best_nvalid = nvalid;
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) saved[u] = raw[u];
-        }
-    }
+    if (mode == kKeysChoose) mode = kKeysExact;      // no group: sign-magnitude keys
 
     packed = pack_kc(KeyTraits<4>::kNone, 0x7fffffff);
     bits = 0;
     if (best_group >= 0) {
         int su, e;
-        if (mode == kKeysRaw) find_first<EB, kKeysRaw>(saved, best_nvalid, best_key, su, e, bits);
+        if (mode == kKeysRaw) find_first<EB, kKeysRaw>(saved, best_key, su, e, bits);
         else if (mode == kKeysExact)
-            find_first<EB, kKeysExact>(saved, best_nvalid, best_key, su, e, bits);
-        else find_first<EB, kKeysNan>(saved, best_nvalid, best_key, su, e, bits);
+            find_first<EB, kKeysExact>(saved, best_key, su, e, bits);
+        else find_first<EB, kKeysNan>(saved, best_key, su, e, bits);
         const int64_t vi = (int64_t)t.v0 + best_group * kGroupVecs + su * kRowThreads + t.tid;
         packed = pack_kc(best_key, col_base + vi * kEpv + e);
     }
@@ -564,7 +545,7 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
     t.v0 = (int32_t)(split * chunk_vecs);
     t.v1 = (int32_t)min(split * chunk_vecs + chunk_vecs, geom.nvec);
     t.nv = t.v1 > t.v0 ? t.v1 - t.v0 : 0;
-    t.nfull = t.nv / kGroupVecs;
+    t.ngroups = (t.nv + kGroupVecs - 1) / kGroupVecs;
     t.tid = tid;
     const int64_t col_base = col_offset + geom.head;
 
@@ -682,10 +663,11 @@ __device__ __forceinline__ void row_tile(
 
 // The row pass as its own kernel, followed by the scan kernel.  Block 0 also
 // writes the packed row offsets of the requests when `packed_offsets` is set.
-// Six wavefronts per SIMD: the two load buffers fit in 80 VGPRs with no spill
-// (a tighter budget spills).
+// Five wavefronts per SIMD: the two load buffers and the clamped offsets of
+// the last group fit in 96 VGPRs with no spill (at six, 80 VGPRs, the kernel
+// spills to scratch and runs 25% slower).
 template <int EB>
-__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(6))) void asd_row_kernel(
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(5))) void asd_row_kernel(
     const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
     int64_t chunk_vecs, const int32_t* __restrict__ draft_tokens,
     TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
@@ -1510,6 +1492,71 @@ __global__ void asd_fill_u64_kernel(unsigned long long* p, int64_t n, unsigned l
     if (i < n) p[i] = v;
 }
 
+// ------------------------------------------------------- matrix-core probe
+//
+// The matrix-core work of asd_lmhead_kernel with no memory traffic: a
+// workgroup of eight wavefronts, each wavefront issuing 32
+// v_mfma_f32_32x32x16_bf16 per K step of 64 into its 4 x 2 accumulator tiles,
+// as the LM-head kernel does, with operand fragments held in registers.  Each
+// thread reads six fragments once from the caller's buffer and forms four
+// fragment sets from them (the elements rotated within each fragment), which
+// the steps cycle through, so that the matrix cores see data of the caller's
+// distribution (the power a matrix core draws depends on its operands' bits).
+// Workgroup w reads the data of workgroup w % 64, which then stays in the
+// cache.  Run over as many workgroups and steps as an LM-head launch, its
+// duration is the practical matrix-core ceiling of that launch under the
+// chip's power limit.  Thread 0 of each workgroup writes the binary32 bits of
+// the sum of its accumulators.
+constexpr int kProbeSets = 4;
+constexpr int kProbeVecs = 6;                  // 16-byte fragments read per thread
+
+template <int R>
+__device__ __forceinline__ bf16x8 rotate_elements(bf16x8 v) {
+    return __builtin_shufflevector(v, v, R % 8, (R + 1) % 8, (R + 2) % 8, (R + 3) % 8,
+                                   (R + 4) % 8, (R + 5) % 8, (R + 6) % 8, (R + 7) % 8);
+}
+
+__global__ __launch_bounds__(kLmThreads) void asd_mfma_probe_kernel(
+    const bf16x8* __restrict__ operands, int64_t vectors, int64_t steps,
+    uint32_t* __restrict__ out) {
+    bf16x8 a[kProbeSets][4], b[kProbeSets][2];
+    const int64_t first = ((int64_t)(blockIdx.x % 64) * kLmThreads + threadIdx.x) * kProbeVecs;
+    bf16x8 f[kProbeVecs];
+#pragma unroll
+    for (int k = 0; k < kProbeVecs; ++k) f[k] = operands[(first + k) % vectors];
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+        bf16x8* const dst0 = k < 4 ? &a[0][k] : &b[0][k - 4];
+        bf16x8* const dst1 = k < 4 ? &a[1][k] : &b[1][k - 4];
+        bf16x8* const dst2 = k < 4 ? &a[2][k] : &b[2][k - 4];
+        bf16x8* const dst3 = k < 4 ? &a[3][k] : &b[3][k - 4];
+        *dst0 = f[k];
+        *dst1 = rotate_elements<1>(f[k]);
+        *dst2 = rotate_elements<2>(f[k]);
+        *dst3 = rotate_elements<3>(f[k]);
+    }
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16)(0.0f);
+    for (int64_t s = 0; s < steps; ++s) {
+#pragma unroll
+        for (int t = 0; t < kProbeSets; ++t) lm_mfma8(a[t], b[t], acc);
+    }
+    float sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float x = acc[i][j][v];
+                sum += x;
+            }
+    if (threadIdx.x == 0) out[blockIdx.x] = __float_as_uint(sum);
+}
+
 // ------------------------------------------------------- read probe
 //
 // The row kernel's access pattern with no ranking: one workgroup per row,
@@ -1692,6 +1739,13 @@ hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t 
     A.row_best = best;
     A.row_draft_bits = draft_bits;
     return launch_scan(A, true, stream);
+}
+
+hipError_t launch_mfma_probe(const void* operands, int64_t vectors, int64_t workgroups,
+                             int64_t steps, uint32_t* out, hipStream_t stream) {
+    asd_mfma_probe_kernel<<<(unsigned)workgroups, kLmThreads, 0, stream>>>(
+        (const bf16x8*)operands, vectors, steps, out);
+    return hipGetLastError();
 }
 
 hipError_t launch_read_probe(const void* buf, int64_t rows, int64_t row_bytes, uint32_t* out,

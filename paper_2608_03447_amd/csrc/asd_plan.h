@@ -165,6 +165,11 @@ hipError_t launch_lmhead_verify(const void* hidden, const void* weight, int64_t 
                                 int64_t vocab, int64_t rows, const CallArgs& a, void* workspace,
                                 hipStream_t stream);
 
+// Matrix-core probe: `workgroups` workgroups of the LM-head kernel's shape, each
+// running `steps` K steps of its MFMA work on operands held in registers.
+hipError_t launch_mfma_probe(const void* operands, int64_t vectors, int64_t workgroups,
+                             int64_t steps, uint32_t* out, hipStream_t stream);
+
 // Read probe: `rows` workgroups each streaming `row_bytes` (a multiple of 16)
 // from a 16-byte aligned buffer.
 hipError_t launch_read_probe(const void* buf, int64_t rows, int64_t row_bytes, uint32_t* out,

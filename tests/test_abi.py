@@ -357,3 +357,13 @@ def test_binding_rejects_strided_or_misplaced_vectors():
     with pytest.raises(ValueError, match="row_offsets"):
         asd.asd_opportunity(draft, amax, regret, 100, lens, taus, ps, counts, mism,
                             row_offsets=strided64)
+
+
+@pytest.mark.parametrize("args", [
+    (None, 24, 1, 1), (0x1008, 24, 1, 1), (0x1000, 5, 1, 1), (0x1000, 24, 0, 1),
+    (0x1000, 24, 1 << 31, 1), (0x1000, 24, 1, 0)])
+def test_mfma_probe_rejects_invalid_arguments(args):
+    lib = asd._load()
+    ops, vectors, wgs, steps = args
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    assert lib.asd_mfma_probe(vp(ops), vectors, wgs, steps, vp(0x2000), None) == 1

@@ -29,3 +29,16 @@ def test_read_probe_folds_every_vector(rows, vecs):
         asd.asd_read_probe(buf, rows, row_bytes, out)
         torch.cuda.synchronize()
         assert out.item() == int(MARK), (r, v)
+
+
+@pytest.mark.parametrize("workgroups,steps", [(1, 1), (3, 5), (300, 2)])
+def test_mfma_probe_runs_every_step(workgroups, steps):
+    """With every operand 1.0 each accumulator of thread 0 ends at 64 * steps,
+    so its 128 accumulators sum to 8192 * steps (exact in binary32)."""
+    print("mfma probe workgroups %d steps %d" % (workgroups, steps), flush=True)
+    ops = torch.ones(24 * 8 * 4, dtype=torch.bfloat16, device=DEV)
+    out = torch.zeros(workgroups, dtype=torch.int32, device=DEV)
+    asd.asd_mfma_probe(ops, workgroups, steps, out)
+    torch.cuda.synchronize()
+    expect = np.array([8192.0 * steps], dtype=np.float32).view(np.int32)[0]
+    assert (out.cpu().numpy() == expect).all()
