@@ -73,6 +73,23 @@ int main() {
     expect(asd_verify_ex(L, ASD_BF16, 100, 0, 0, D, K, nullptr, T, M, B, A, X, nullptr, nullptr,
                          ASD_GATE_RAW, nullptr, nullptr, 0), ASD_OK, "verify_ex empty");
     expect(asd_device_error(nullptr, 1, nullptr), ASD_EINVAL, "device_error null output");
+    expect(asd_verify_static(nullptr, ASD_BF16, 100, 1, 2, D, K, nullptr, T, M, B, A, X, nullptr,
+                             nullptr, nullptr),
+           ASD_EINVAL, "verify_static null logits");
+    expect(asd_verify_static(L, 9, 100, 1, 2, D, K, nullptr, T, M, B, A, X, nullptr, nullptr,
+                             nullptr),
+           ASD_EDTYPE, "verify_static bad dtype");
+    expect(asd_verify_static(L, ASD_F32, 100, 0, 0, nullptr, nullptr, nullptr, nullptr, nullptr,
+                             nullptr, nullptr, nullptr, nullptr, nullptr, nullptr),
+           ASD_OK, "verify_static empty batch");
+    expect(asd_mfma_probe(nullptr, 24, 1, 1, fake<uint32_t>(0xe0000), nullptr), ASD_EINVAL,
+           "mfma_probe null operands");
+    expect(asd_mfma_probe(fake<const void>(0x10008), 24, 1, 1, fake<uint32_t>(0xe0000), nullptr),
+           ASD_EINVAL, "mfma_probe misaligned");
+    expect(asd_mfma_probe(L, 5, 1, 1, fake<uint32_t>(0xe0000), nullptr), ASD_EINVAL,
+           "mfma_probe too few vectors");
+    expect(asd_mfma_probe(L, 24, 1, 0, fake<uint32_t>(0xe0000), nullptr), ASD_EINVAL,
+           "mfma_probe no steps");
 
     // sharded form
     expect(asd_shard_argmax(L, ASD_BF16, 0, 0, 100, 2, D, fake<asd_row_partial>(0xa0000),
@@ -106,7 +123,7 @@ int main() {
     for (int64_t v : {1, 7, 8, 32000, 151936})
         for (int64_t rows : {1, 9, 544, 4352})
             (void)asd_workspace_bytes(ASD_BF16, v, (int32_t)(rows > 4 ? rows / 4 : 1), rows);
-    for (int c = -1; c <= 6; ++c) (void)asd_status_string(c);
+    for (int c = -1; c <= 7; ++c) (void)asd_status_string(c);
     expect(asd_verify(L, 7, 100, 1, 2, D, K, nullptr, T, M, B, A, X, nullptr, nullptr, nullptr),
            ASD_EDTYPE, "verify dtype 7");
     (void)asd_version();
@@ -138,6 +155,13 @@ int main() {
         if (e != ASD_EHIP) {
             std::fprintf(stderr, "device_error without a device returned %s\n",
                          asd_status_string(e));
+            ++failures;
+        }
+        const asd_status v = asd_verify_static(L, ASD_BF16, 100, 1, 2, D, K, nullptr, T, M, B, A,
+                                               X, nullptr, nullptr, nullptr);
+        if (v != ASD_EHIP) {
+            std::fprintf(stderr, "verify_static without a device returned %s\n",
+                         asd_status_string(v));
             ++failures;
         }
         const asd_status t = asd_lmhead_verify(L, L, 256, 100, 1, 2, D, K, nullptr, T, M, B, A,

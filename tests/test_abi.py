@@ -37,14 +37,14 @@ def test_status_strings_and_version():
     assert "gfx950" in asd.asd_version()
 
 
-def _call(**kw):
+def _call(entry="asd_verify", **kw):
     lib = asd._load()
     a = dict(logits=0x1000, dtype=1, vocab=100, nreq=1, rows=2, draft=0x2000, lens=0x3000,
              offs=None, tau=0x4000, cap=0x5000, budget=0x6000, acc=0x7000, nxt=0x8000,
              amax=None, regret=None, stream=None)
     a.update(kw)
     vp = lambda v: None if v is None else ctypes.c_void_p(v)
-    return lib.asd_verify(vp(a["logits"]), a["dtype"], a["vocab"], a["nreq"], a["rows"],
+    return getattr(lib, entry)(vp(a["logits"]), a["dtype"], a["vocab"], a["nreq"], a["rows"],
                           vp(a["draft"]), vp(a["lens"]), vp(a["offs"]), vp(a["tau"]),
                           vp(a["cap"]), vp(a["budget"]), vp(a["acc"]), vp(a["nxt"]),
                           vp(a["amax"]), vp(a["regret"]), vp(a["stream"]))
@@ -68,12 +68,19 @@ def _call(**kw):
     (dict(logits=0x1001), 1),                  # not a multiple of the bf16 size
     (dict(dtype=0, logits=0x1002), 1),         # not a multiple of the f32 size
 ])
-def test_invalid_arguments_are_rejected_without_launch(kw, status):
-    assert _call(**kw) == status
+@pytest.mark.parametrize("entry", ["asd_verify", "asd_verify_static"])
+def test_invalid_arguments_are_rejected_without_launch(kw, status, entry):
+    assert _call(entry, **kw) == status
 
 
-def test_empty_batch_is_a_no_op():
-    assert _call(nreq=0, rows=0, logits=None, draft=None) == 0
+@pytest.mark.parametrize("entry", ["asd_verify", "asd_verify_static"])
+def test_empty_batch_is_a_no_op(entry):
+    assert _call(entry, nreq=0, rows=0, logits=None, draft=None) == 0
+
+
+def test_static_scratch_size_and_status_string():
+    assert asd.ASD_STATIC_SCRATCH_BYTES == 4 << 20
+    assert "ESCRATCH" in asd.asd_status_string(asd.ASD_ESCRATCH)
 
 
 def test_workspace_bytes_rejects_invalid_shapes():
