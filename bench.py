@@ -433,14 +433,16 @@ def main():
     log("timed %d calls: %.3f ms total, %.1f us/call, wall %.3fs" % (
         args.steps, total_ms, ms_per_step * 1e3, wall))
 
-    # The dominant kernel alone: asd_shard_argmax over the whole rows (offset 0,
-    # width V) is the same row kernel with the same grid as the call above,
-    # writing a 16-byte partial per row instead of an 8-byte record.
+    # The dominant kernel alone: asd_row_pass is the same row kernel on the same
+    # tile grid as the call above (S tiles per row), each tile writing a
+    # 16-byte partial (the call writes an 8-byte record per row when S = 1).
     row_only = None
     if args.shards == 0 and w.blocks == 1 and w.num_requests > 0:
-        parts_full = torch.empty((w.rows_per_call, 4), dtype=torch.int32, device=dev)
+        splits = asd.asd_row_splits(logits.dtype, w.vocab, w.rows_per_call)
+        parts_full = torch.empty((w.rows_per_call, splits, 4), dtype=torch.int32, device=dev)
+        row_pass = lambda: asd.asd_row_pass(logits, draft, out_partials=parts_full)
         for _ in range(3):
-            asd.asd_shard_argmax(logits, 0, w.vocab, draft, out_partials=parts_full)
+            row_pass()
         r0 = torch.cuda.Event(enable_timing=True)
         r1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -452,7 +454,7 @@ def main():
                 a0 = torch.cuda.Event(enable_timing=True)
                 a1 = torch.cuda.Event(enable_timing=True)
                 a0.record(stream)
-                asd.asd_shard_argmax(logits, 0, w.vocab, draft, out_partials=parts_full)
+                row_pass()
                 a1.record(stream)
                 spans.append((a0, a1))
             torch.cuda.synchronize()
@@ -461,18 +463,19 @@ def main():
         else:
             r0.record(stream)
             for _ in range(args.steps):
-                asd.asd_shard_argmax(logits, 0, w.vocab, draft, out_partials=parts_full)
+                row_pass()
             r1.record(stream)
             torch.cuda.synchronize()
             row_ms = r0.elapsed_time(r1) / args.steps
         row_bytes = w.logit_bytes_per_call + 4 * w.rows_per_call
         row_only = {"kernel": "asd_row_kernel (one workgroup per row tile, as in the call)",
+                    "tiles_per_row": splits,
                     "avg_launch_ms": row_ms,
                     "algorithmic_bytes_per_launch": row_bytes,
                     "achieved": row_bytes / (row_ms / 1e3) / 1e9,
                     "frac": row_bytes / (row_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-                    "note": "timed with HIP events around asd_shard_argmax(offset 0, width V), "
-                            "the verifier's row pass alone"}
+                    "note": "timed with HIP events around asd_row_pass, the verifier's row "
+                            "pass alone on the call's tile grid"}
         log("row kernel alone: %.1f us, %.0f GB/s" % (row_ms * 1e3, row_only["achieved"]))
 
     def timed_calls(fn, count, evict_first):

@@ -418,6 +418,36 @@ asd_status asd_lmhead_verify(const void *hidden, const void *weight, int64_t d, 
                              int32_t *out_argmax, float *out_regret, void *stream);
 
 /*
+ * asd_row_splits -- the number S of column tiles per row that asd_verify cuts
+ * `total_rows` rows of `vocab` elements of `dtype` into on the current device
+ * (its row pass runs one workgroup per tile).  0 for arguments asd_verify
+ * rejects (dtype, vocab outside [1, 2^30), total_rows outside [1, 2^31)).
+ */
+int32_t asd_row_splits(asd_dtype dtype, int64_t vocab, int64_t total_rows);
+
+/*
+ * asd_row_pass -- a measurement helper: the first stage of asd_verify alone
+ * (each row's greatest logit with its column, Eq. 1, and the draft token's
+ * logit, Eq. 3), as the same row kernel on the same tile grid that asd_verify
+ * launches for these rows: S = asd_row_splits(dtype, vocab, total_rows) tiles
+ * per row, one workgroup per tile.  Its duration is that stage's duration
+ * inside asd_verify; the only difference is that every tile writes a 16-byte
+ * partial (asd_verify writes an 8-byte row record when S = 1).
+ *
+ * logits, dtype, vocab, total_rows, draft_tokens: as for asd_verify (the rows
+ *                 are the rows of a packed or explicit-offset batch alike).
+ * out_partials    asd_row_partial [total_rows][S], 16-byte aligned: tile s of
+ *                 row r in entry r * S + s, with the layout asd_shard_argmax
+ *                 writes (opaque).  The tile whose columns hold the draft
+ *                 token holds its logit.
+ * Returns ASD_EDTYPE or ASD_EINVAL for the argument errors asd_shard_argmax
+ * rejects.  Allocates nothing and uses no workspace.  Asynchronous on `stream`.
+ */
+asd_status asd_row_pass(const void *logits, asd_dtype dtype, int64_t vocab, int64_t total_rows,
+                        const int32_t *draft_tokens, asd_row_partial *out_partials,
+                        void *stream);
+
+/*
  * asd_read_probe -- a measurement helper: stream `rows` rows of `row_bytes`
  * bytes from `buf` once, with the access pattern of the verifier's row pass
  * (one 256-thread workgroup per row, 16-byte non-temporal loads, four per lane

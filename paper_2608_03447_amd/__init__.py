@@ -15,7 +15,8 @@ from .build import HASHED_SOURCES, LIBRARY, source_hash
 
 __all__ = ["asd_verify", "asd_verify_static", "asd_verify_ws", "asd_verify_ex", "asd_shard_argmax",
            "asd_verify_partials", "asd_opportunity", "asd_commit", "asd_verify_commit",
-           "asd_lmhead_verify", "asd_device_error", "asd_read_probe", "asd_mfma_probe", "asd_workspace_bytes",
+           "asd_lmhead_verify", "asd_device_error", "asd_row_splits", "asd_row_pass", "asd_read_probe",
+           "asd_mfma_probe", "asd_workspace_bytes",
            "asd_status_string", "asd_version", "asd_release", "AsdError", "ASD_F32", "ASD_BF16",
            "ASD_GATE_RAW", "ASD_DEVERR_NEGATIVE_K", "ASD_DEVERR_ROWS", "ASD_DEVERR_COMMIT",
            "library_path", "library_source_hash", "check_built_from_sources"]
@@ -84,6 +85,10 @@ def _load():
     lib.asd_device_error.restype = ctypes.c_int
     lib.asd_mfma_probe.argtypes = [vp, i64, i64, i64, vp, vp]
     lib.asd_mfma_probe.restype = ctypes.c_int
+    lib.asd_row_splits.argtypes = [ctypes.c_int, i64, i64]
+    lib.asd_row_splits.restype = i32
+    lib.asd_row_pass.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, vp]
+    lib.asd_row_pass.restype = ctypes.c_int
     lib.asd_read_probe.argtypes = [vp, i64, i64, vp, vp]
     lib.asd_read_probe.restype = ctypes.c_int
     lib.asd_shard_argmax.argtypes = [vp, ctypes.c_int, i64, i64, i64, i64, vp, vp, vp]
@@ -299,6 +304,50 @@ def asd_device_error(clear=False, device=None) -> int:
     if st != 0:
         raise AsdError(st, "asd_device_error")
     return int(word.value)
+
+
+def asd_row_splits(dtype, vocab, total_rows):
+    """Column tiles per row of asd_verify's row pass on the current device
+    (``asd_row_splits``); ``dtype`` is torch.float32 or torch.bfloat16."""
+    if dtype not in _DTYPES:
+        raise ValueError("dtype must be torch.float32 or torch.bfloat16")
+    return int(_load().asd_row_splits(_DTYPES[dtype], int(vocab), int(total_rows)))
+
+
+def asd_row_pass(logits, draft_tokens, out_partials=None):
+    """asd_verify's row pass alone, on the call's own tile grid (``asd_row_pass``).
+
+    logits        [total_rows, V] float32 or bfloat16, contiguous, on a GPU
+    draft_tokens  int32 [total_rows]
+    Returns the partials, an int32 tensor [total_rows, S, 4] (16 opaque bytes
+    per tile, S = asd_row_splits)."""
+    if logits.dim() != 2 or logits.dtype not in _DTYPES or not logits.is_cuda:
+        raise ValueError("logits must be a 2-D float32 or bfloat16 tensor on a GPU")
+    if not logits.is_contiguous():
+        raise ValueError("logits must be contiguous (row-major, dense)")
+    dev = logits.device
+    rows, vocab = logits.shape
+    if draft_tokens.dtype != torch.int32 or draft_tokens.shape != (rows,) \
+            or draft_tokens.device != dev:
+        raise ValueError("draft_tokens must be int32 of shape (%d,) on %s" % (rows, dev))
+    with torch.cuda.device(dev):
+        splits = asd_row_splits(logits.dtype, vocab, rows)
+        if splits < 1:
+            raise ValueError("no row pass for %d rows of %d columns" % (rows, vocab))
+        if out_partials is None:
+            out_partials = torch.empty((rows, splits, 4), dtype=torch.int32, device=dev)
+        if out_partials.dtype != torch.int32 or out_partials.shape != (rows, splits, 4) \
+                or not out_partials.is_contiguous() or out_partials.device != dev:
+            raise ValueError("out_partials must be a contiguous int32 (%d, %d, 4) tensor on %s"
+                             % (rows, splits, dev))
+        draft_tokens = draft_tokens.contiguous()
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        st = _load().asd_row_pass(ctypes.c_void_p(logits.data_ptr()), _DTYPES[logits.dtype],
+                                  vocab, rows, ctypes.c_void_p(draft_tokens.data_ptr()),
+                                  ctypes.c_void_p(out_partials.data_ptr()), ctypes.c_void_p(stream))
+    if st != 0:
+        raise AsdError(st, "asd_row_pass")
+    return out_partials
 
 
 def asd_read_probe(buf, rows, row_bytes, out_word):

@@ -402,6 +402,34 @@ asd_status asd_shard_argmax(const void* shard_logits, asd_dtype dtype, int64_t s
                : ASD_EHIP;
 }
 
+int32_t asd_row_splits(asd_dtype dtype, int64_t vocab, int64_t total_rows) {
+    if (elem_bytes_of(dtype) == 0 || vocab < 1 || vocab >= ((int64_t)1 << 30) ||
+        total_rows < 1 || total_rows >= ((int64_t)1 << 31))
+        return 0;
+    Plan plan;
+    if (plan_for(dtype, vocab, 0, total_rows, &plan) != ASD_OK) return 0;
+    return plan.splits;
+}
+
+asd_status asd_row_pass(const void* logits, asd_dtype dtype, int64_t vocab, int64_t total_rows,
+                        const int32_t* draft_tokens, asd_row_partial* out_partials,
+                        void* stream) {
+    const int eb = elem_bytes_of(dtype);
+    if (eb == 0) return ASD_EDTYPE;
+    if (vocab < 1 || vocab >= ((int64_t)1 << 30)) return ASD_EINVAL;
+    if (total_rows < 1 || total_rows >= ((int64_t)1 << 31)) return ASD_EINVAL;
+    if (!logits || !draft_tokens || !out_partials) return ASD_EINVAL;
+    if (((uintptr_t)logits % (uintptr_t)eb) != 0 || ((uintptr_t)out_partials & 15) != 0)
+        return ASD_EINVAL;
+    Plan plan;
+    asd_status st;
+    if ((st = plan_for(dtype, vocab, 0, total_rows, &plan)) != ASD_OK) return st;
+    return launch_row_pass(plan, logits, draft_tokens, out_partials, (hipStream_t)stream) ==
+                   hipSuccess
+               ? ASD_OK
+               : ASD_EHIP;
+}
+
 asd_status asd_verify_partials(const asd_row_partial* partials, int32_t num_shards,
                                int64_t shard_vocab, int64_t vocab, int32_t num_requests,
                                int64_t total_rows, const int32_t* draft_tokens,

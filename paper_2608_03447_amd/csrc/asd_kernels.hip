@@ -293,7 +293,7 @@ __device__ __forceinline__ RowGeom row_geom(const unsigned char* row_ptr, int64_
 __device__ __forceinline__ int owner_split(int64_t c, const RowGeom& g, int64_t chunk_cols,
                                            int splits) {
     if (c < g.head) return 0;
-    const int64_t s = (c - g.head) / chunk_cols;
+    const int64_t s = (uint32_t)(c - g.head) / (uint32_t)chunk_cols;   // both below 2^31
     return s < splits - 1 ? (int)s : splits - 1;
 }
 
@@ -448,10 +448,10 @@ constexpr int kKeysChoose = 3;
 // in [1, +inf] in any lane, else switches to sign-magnitude keys (ranking the
 // group again from its registers).  Except with NaN keys, `umax` takes the
 // greatest pattern read as unsigned (per 16-bit half for bf16).
-template <int EB>
+template <int EB, typename Hook>
 __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t col_base,
                                            unsigned long long& packed, uint32_t& bits,
-                                           uint32_t& umax) {
+                                           uint32_t& umax, Hook&& after_first_loads) {
     constexpr int kEpv = 16 / EB;
     int32_t best_key = KeyTraits<4>::kNone;
     int32_t best_group = -1;
@@ -483,11 +483,16 @@ __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t 
     // Whole groups through two register buffers in ping-pong: a group's four
     // loads are issued before the previous group is ranked, so each wavefront
     // keeps eight 16-byte loads per lane in flight while it computes.  The
+    // first two groups are issued before anything else that reads memory (the
+    // hook), so a tile's first data is requested as soon as it starts.  The
     // scheduling barriers keep the compiler from moving ranking work (and its
     // waits) ahead of the loads.
     if (t.ngroups > 0) {
         u32x4 ra[kUnroll], rb[kUnroll];
         load_group(t, ra, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        after_first_loads();
+        __builtin_amdgcn_sched_barrier(0);
         int32_t g = 0;
         for (; g + 2 < t.ngroups; g += 2) {
             load_group(t, rb, g + 1);
@@ -505,6 +510,8 @@ __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t 
         } else {
             rank_group(ra, g);
         }
+    } else {
+        after_first_loads();
     }
     if (mode == kKeysChoose) mode = kKeysExact;      // no group: sign-magnitude keys
 
@@ -533,12 +540,12 @@ __device__ __forceinline__ void rank_share(const TileSpan& t, int mode, int64_t 
 // that the greatest key does not show (one with the sign bit set, or any NaN
 // among the head and tail elements).
 // kNanPass = true: NaN keys, for a tile known to hold a NaN.
-template <int EB, bool kNanPass>
+template <int EB, bool kNanPass, typename Hook>
 __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const RowGeom& geom,
                                           int64_t vocab, int64_t col_offset, int split,
                                           int splits, int64_t chunk_vecs, int tid,
                                           unsigned long long& packed, uint32_t& bits,
-                                          bool& nan_seen) {
+                                          bool& nan_seen, Hook&& after_first_loads) {
     constexpr int kScalarMode = kNanPass ? kKeysNan : kKeysExact;
     TileSpan t;
     t.vec = (const u32x4*)(row_ptr + geom.head * EB);
@@ -551,9 +558,9 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
 
     uint32_t umax = 0;
     if constexpr (kNanPass) {
-        rank_share<EB>(t, kKeysNan, col_base, packed, bits, umax);
+        rank_share<EB>(t, kKeysNan, col_base, packed, bits, umax, after_first_loads);
     } else {
-        rank_share<EB>(t, kKeysChoose, col_base, packed, bits, umax);
+        rank_share<EB>(t, kKeysChoose, col_base, packed, bits, umax, after_first_loads);
         if constexpr (EB == 2)
             nan_seen = max(umax & 0xffffu, umax >> 16) > KeyTraits<2>::kNegInfPattern;
         else
@@ -585,13 +592,14 @@ __device__ __forceinline__ void tile_best(const unsigned char* row_ptr, const Ro
 // = 0 and vocab = V unless the rows are one tensor-parallel shard); columns are
 // reported globally.  With `partials` set the tile writes a partial (split
 // rows, or one shard of each row); otherwise the row is one tile and writes its
-// record.  Thread 0 writes; every thread returns.
-template <int EB>
+// record.  `pre` runs once, right after the tile's first loads are issued (for
+// the caller's own loads).  Thread 0 writes; every thread returns.
+template <int EB, typename Pre>
 __device__ __forceinline__ void row_tile(
     const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
     int64_t chunk_vecs, const int32_t* __restrict__ draft_tokens,
     TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
-    int32_t* __restrict__ out_argmax) {
+    int32_t* __restrict__ out_argmax, Pre&& pre) {
     constexpr int kEpv = 16 / EB;
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x / splits;
@@ -600,17 +608,24 @@ __device__ __forceinline__ void row_tile(
     const RowGeom geom = row_geom(row_ptr, vocab, EB);
     const int64_t chunk_cols = chunk_vecs * kEpv;
 
-    // Draft token of this row (uniform); the owning tile gathers z(x) early so
-    // the load overlaps the stream.
-    const int32_t x = draft_tokens[row];
-    const int64_t x_local = (int64_t)x - col_offset;
-    const bool x_here = x_local >= 0 && x_local < vocab;
-    const bool owns_x = x_here && owner_split(x_local, geom, chunk_cols, splits) == split;
-    uint32_t draft_bits = 0;
-    if (owns_x && tid == 0) {
-        int32_t k_unused;
-        load_scalar<EB, kKeysRaw>(row_ptr + x_local * EB, k_unused, draft_bits);
-    }
+    // The row's draft token x (uniform) and, in the tile that owns its column,
+    // the pattern of z(x).  Both are read after the tile's first loads are
+    // issued.  Every lane reads the pattern from one uniform address (the row's
+    // first element when the tile does not own x): with no branch around the
+    // load nothing waits for it before the ranking, so it overlaps the stream.
+    int32_t x = 0;
+    bool x_here = false, owns_x = false;
+    uint32_t draft_raw = 0;
+    auto after_first_loads = [&]() {
+        x = draft_tokens[row];
+        const int64_t x_local = (int64_t)x - col_offset;
+        x_here = x_local >= 0 && x_local < vocab;
+        owns_x = x_here && owner_split(x_local, geom, chunk_cols, splits) == split;
+        const unsigned char* p = row_ptr + (owns_x ? x_local * EB : 0);
+        if constexpr (EB == 2) draft_raw = *(const unsigned short*)p;
+        else draft_raw = *(const uint32_t*)p;
+        pre();
+    };
 
     // ---- rank the tile (first pass); if it holds a NaN, rank it again to find
     // its first NaN.
@@ -618,7 +633,7 @@ __device__ __forceinline__ void row_tile(
     uint32_t bits;
     bool nan_seen = false;
     tile_best<EB, false>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid, packed,
-                         bits, nan_seen);
+                         bits, nan_seen, after_first_loads);
     __shared__ int s_nan[kWaves];
     const bool wave_nan = __ballot(nan_seen) != 0ull;
     if ((tid & 63) == 0) s_nan[tid >> 6] = wave_nan;
@@ -633,10 +648,11 @@ __device__ __forceinline__ void row_tile(
     __syncthreads();
     if (s_again) {
         tile_best<EB, true>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
-                            packed, bits, nan_seen);
+                            packed, bits, nan_seen, [] {});
         block_reduce(packed, bits);
     }
     if (tid != 0) return;
+    const uint32_t draft_bits = owns_x ? (EB == 2 ? draft_raw << 16 : draft_raw) : 0u;
 
     if (partials != nullptr) {           // combined by the scan
         TilePartial tp;
@@ -662,10 +678,12 @@ __device__ __forceinline__ void row_tile(
 }
 
 // The row pass as its own kernel, followed by the scan kernel.  Block 0 also
-// writes the packed row offsets of the requests when `packed_offsets` is set.
-// Five wavefronts per SIMD: the two load buffers and the clamped offsets of
-// the last group fit in 96 VGPRs with no spill (at six, 80 VGPRs, the kernel
-// spills to scratch and runs 25% slower).
+// writes the packed row offsets of the requests when `packed_offsets` is set,
+// after its first loads are issued: a test of that argument ahead of the row
+// pass would make every tile wait for its arguments twice before its first
+// load.  Five wavefronts per SIMD: the two load buffers and the clamped offsets
+// of the last group fit in 96 VGPRs with no spill (at six, 80 VGPRs, an
+// earlier form spilled to scratch and ran 25% slower).
 template <int EB>
 __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(5))) void asd_row_kernel(
     const unsigned char* __restrict__ logits, int64_t vocab, int64_t col_offset, int splits,
@@ -673,10 +691,11 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(5))
     TilePartial* __restrict__ partials, RowRecord* __restrict__ records,
     int32_t* __restrict__ out_argmax, int32_t num_requests,
     const int32_t* __restrict__ block_lens, int64_t* __restrict__ packed_offsets) {
-    if (packed_offsets != nullptr && blockIdx.x == 0)
-        write_packed_offsets(num_requests, block_lens, packed_offsets);
     row_tile<EB>(logits, vocab, col_offset, splits, chunk_vecs, draft_tokens, partials, records,
-                 out_argmax);
+                 out_argmax, [&] {
+                     if (blockIdx.x == 0 && packed_offsets != nullptr)
+                         write_packed_offsets(num_requests, block_lens, packed_offsets);
+                 });
 }
 
 // ----------------------------------------------------------- stage 2 kernel
@@ -954,13 +973,14 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_scan_kernel(const unsigne
                     int64_t chunk_vecs, TilePartial* __restrict__ partials,
                     RowRecord* __restrict__ records, unsigned* __restrict__ counter,
                     const ScanArgs A) {
-    // The requests' inputs and row offsets are loaded before the row pass (the
-    // few requests of a single-launch plan: wavefront w takes requests w and
-    // w + 4), so that the last tile's scan waits only for the rows.
+    // Every tile loads the requests' inputs and row offsets during its row pass,
+    // right after its first loads are issued (the few requests of a
+    // single-launch plan: wavefront w takes requests w and w + 4), so that the
+    // last tile's scan waits only for the rows.
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     RequestIn q[2];
     int64_t o[2];
-    {
+    auto preload = [&]() {
         const int n = A.num_requests;            // <= kSingleLaunchMaxRequests <= 64
         const int32_t Kl = lane < n ? A.block_lens[lane] : 0;
         long long incl = lane < n ? (long long)(Kl > 0 ? Kl : 0) + 1 : 0;
@@ -978,9 +998,9 @@ __global__ __launch_bounds__(kRowThreads) void asd_row_scan_kernel(const unsigne
                 o[j] = A.offsets ? A.offsets[k] : (int64_t)__shfl(excl, k, 64);
             }
         }
-    }
+    };
     row_tile<EB>(logits, vocab, 0, splits, chunk_vecs, A.draft_tokens, partials, records,
-                 splits == 1 ? A.out_argmax : nullptr);
+                 splits == 1 ? A.out_argmax : nullptr, preload);
     __shared__ int s_last;
     if (threadIdx.x == 0) {
         const unsigned prev =
@@ -1636,6 +1656,15 @@ hipError_t launch_verify(const Plan& plan, const CallArgs& a, void* workspace,
     A.partials = partials;
     A.shard_vocab = 0;
     return launch_scan(A, plan.splits > 1, stream);
+}
+
+hipError_t launch_row_pass(const Plan& plan, const void* logits, const int32_t* draft_tokens,
+                          void* out_partials, hipStream_t stream) {
+    return launch_row(plan.elem_bytes, dim3((unsigned)(plan.rows * plan.splits)), stream,
+                      (const unsigned char*)logits, plan.vocab, (int64_t)0, plan.splits,
+                      plan.chunk_vecs, draft_tokens, (TilePartial*)out_partials,
+                      (RowRecord*)nullptr, (int32_t*)nullptr, (int32_t)0,
+                      (const int32_t*)nullptr, (int64_t*)nullptr);
 }
 
 hipError_t launch_shard_argmax(int elem_bytes, const void* shard_logits, int64_t shard_vocab,

@@ -113,6 +113,11 @@ constexpr size_t kCounterHeaderBytes = 256;
 hipError_t launch_verify(const Plan& plan, const CallArgs& args, void* workspace,
                          unsigned* counter, hipStream_t stream);
 
+// The row pass of `plan` alone: the row kernel on the plan's tile grid, every
+// tile writing its TilePartial at out_partials[row * splits + split].
+hipError_t launch_row_pass(const Plan& plan, const void* logits, const int32_t* draft_tokens,
+                          void* out_partials, hipStream_t stream);
+
 // One vocabulary shard: rows of `shard_vocab` columns that are columns
 // [vocab_offset, vocab_offset + shard_vocab) of the full vocabulary.  Writes one
 // TilePartial per row.

@@ -99,6 +99,18 @@ int main() {
     expect(asd_verify_partials(nullptr, 2, 50, 100, 1, 2, D, K, nullptr, T, M, B, A, X, nullptr,
                                nullptr, nullptr), ASD_EINVAL, "partials null");
 
+    // the row pass alone
+    expect(asd_row_pass(L, ASD_BF16, 0, 2, D, fake<asd_row_partial>(0xa0000), nullptr),
+           ASD_EINVAL, "row pass vocab 0");
+    expect(asd_row_pass(L, ASD_BF16, 100, 2, D, fake<asd_row_partial>(0xa0008), nullptr),
+           ASD_EINVAL, "row pass misaligned partials");
+    expect(asd_row_pass(L, (asd_dtype)7, 100, 2, D, fake<asd_row_partial>(0xa0000), nullptr),
+           ASD_EDTYPE, "row pass dtype");
+    if (asd_row_splits((asd_dtype)7, 100, 2) != 0 || asd_row_splits(ASD_BF16, 100, 0) != 0) {
+        std::fprintf(stderr, "FAIL row splits of invalid shapes\n");
+        return 1;
+    }
+
     // opportunity and commit
     const float taus[2] = {0.5f, 1.0f};
     const int32_t ps[2] = {0, 1};

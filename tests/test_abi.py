@@ -374,3 +374,35 @@ def test_mfma_probe_rejects_invalid_arguments(args):
     ops, vectors, wgs, steps = args
     vp = lambda v: None if v is None else ctypes.c_void_p(v)
     assert lib.asd_mfma_probe(vp(ops), vectors, wgs, steps, vp(0x2000), None) == 1
+
+
+def _row_pass(**kw):
+    lib = asd._load()
+    a = dict(logits=0x1000, dtype=1, vocab=100, rows=2, draft=0x2000, out=0x3000, stream=None)
+    a.update(kw)
+    vp = lambda v: None if v is None else ctypes.c_void_p(v)
+    return lib.asd_row_pass(vp(a["logits"]), a["dtype"], a["vocab"], a["rows"], vp(a["draft"]),
+                            vp(a["out"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=5), 2),
+    (dict(vocab=0), 1),
+    (dict(vocab=1 << 30), 1),
+    (dict(rows=0), 1),
+    (dict(rows=1 << 31), 1),
+    (dict(logits=None), 1),
+    (dict(draft=None), 1),
+    (dict(out=None), 1),
+    (dict(out=0x3008), 1),                    # partials must be 16-byte aligned
+    (dict(logits=0x1001), 1),
+    (dict(logits=0x1002, dtype=0), 1),        # f32 rows must be 4-byte aligned
+])
+def test_row_pass_rejects_invalid_arguments(kw, status):
+    assert _row_pass(**kw) == status
+
+
+@pytest.mark.parametrize("args", [(5, 100, 2), (1, 0, 2), (1, 1 << 30, 2), (1, 100, 0),
+                                  (0, 100, 1 << 31)])
+def test_row_splits_is_zero_for_invalid_shapes(args):
+    assert asd._load().asd_row_splits(*args) == 0
