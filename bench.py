@@ -504,17 +504,25 @@ def main():
 
     # Practical read ceiling: the row pass's access pattern with no ranking work
     # (asd_read_probe) over the same logits.
+    # A call that cuts each row into S tiles is compared with the probe over the
+    # same bytes cut into S equal pieces per row (one workgroup each) when the
+    # row divides into 16-byte pieces, else over whole rows.
     practical = None
     row_bytes_v = w.vocab * logits.element_size() if args.shards == 0 else 0
     if (args.shards == 0 and w.blocks == 1 and row_bytes_v % 16 == 0
             and logits.data_ptr() % 16 == 0):
         out_word = torch.zeros(1, dtype=torch.int32, device=dev)
-        probe = lambda: asd.asd_read_probe(logits, w.rows_per_call, row_bytes_v, out_word)
+        probe_tiles = asd.asd_row_splits(logits.dtype, w.vocab, w.rows_per_call)
+        if probe_tiles < 1 or row_bytes_v % (16 * probe_tiles) != 0:
+            probe_tiles = 1
+        probe = lambda: asd.asd_read_probe(logits, w.rows_per_call * probe_tiles,
+                                           row_bytes_v // probe_tiles, out_word)
         for _ in range(3):
             probe()
         d = timed_calls(probe, args.steps, cold)
         p_ms = statistics.mean(d)
         practical = {"kernel": "asd_read_probe (the row pass's loads, no ranking)",
+                     "tiles_per_row": probe_tiles,
                      "avg_launch_ms": p_ms, "bytes_per_launch": w.logit_bytes_per_call,
                      "achieved": w.logit_bytes_per_call / (p_ms / 1e3) / 1e9,
                      "frac": w.logit_bytes_per_call / (p_ms / 1e3) / 1e9 / PEAK_HBM_GBPS}
