@@ -250,26 +250,56 @@ __device__ __forceinline__ void take_better(unsigned long long& p, uint32_t& bit
     }
 }
 
-// Workgroup-wide maximum of (packed, bits); the result is valid in thread 0.
-__device__ __forceinline__ void block_reduce(unsigned long long& p, uint32_t& bits) {
+// One step of a wavefront maximum of (packed, bits) by DPP: each lane takes
+// the pair of the lane that `kCtrl` names when it is greater.  A lane with no
+// source lane in the step (or in a row that kRowMask leaves out) reads 0,
+// which ranks below every packed pair.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ void dpp_max_step(unsigned long long& p, uint32_t& bits) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)p, kCtrl, kRowMask,
+                                                              0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(p >> 32), kCtrl,
+                                                              kRowMask, 0xf, false);
+    const uint32_t qb = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)bits, kCtrl, kRowMask, 0xf,
+                                                              false);
+    const unsigned long long q = ((unsigned long long)hi << 32) | lo;
+    const bool take = q > p;
+    p = take ? q : p;
+    bits = take ? qb : bits;
+}
+
+// Workgroup-wide maximum of (packed, bits), and the OR of one flag per
+// wavefront; every thread returns with both.  Within a wavefront, shifts of 1,
+// 2, 4 and 8 lanes make lane 15 of each 16-lane row hold the row's maximum,
+// and the broadcasts of lanes 15 and 31 carry it on, so that lane 63 holds the
+// wavefront's.  No cross-lane step waits on LDS.  The wavefronts' results meet
+// in LDS behind one barrier.
+__device__ __forceinline__ bool block_reduce(unsigned long long& p, uint32_t& bits, bool flag) {
     __shared__ unsigned long long s_p[kWaves];
     __shared__ uint32_t s_b[kWaves];
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const unsigned long long q = __shfl_xor(p, off, 64);
-        const uint32_t qb = __shfl_xor(bits, off, 64);
-        take_better(p, bits, q, qb);
-    }
+    __shared__ int s_f[kWaves];
+    dpp_max_step<0x111, 0xf>(p, bits);   // row_shr:1
+    dpp_max_step<0x112, 0xf>(p, bits);   // row_shr:2
+    dpp_max_step<0x114, 0xf>(p, bits);   // row_shr:4
+    dpp_max_step<0x118, 0xf>(p, bits);   // row_shr:8
+    dpp_max_step<0x142, 0xa>(p, bits);   // row_bcast:15 into rows 1 and 3
+    dpp_max_step<0x143, 0xc>(p, bits);   // row_bcast:31 into rows 2 and 3
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (lane == 0) {
+    if (lane == 63) {
         s_p[wave] = p;
         s_b[wave] = bits;
+        s_f[wave] = flag;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    p = s_p[0];
+    bits = s_b[0];
+    int any = s_f[0];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) take_better(p, bits, s_p[w], s_b[w]);
+    for (int w = 1; w < kWaves; ++w) {
+        take_better(p, bits, s_p[w], s_b[w]);
+        any |= s_f[w];
     }
+    return any != 0;
 }
 
 __device__ __forceinline__ float bits_to_float(uint32_t b) { return __builtin_bit_cast(float, b); }
@@ -634,22 +664,15 @@ __device__ __forceinline__ void row_tile(
     bool nan_seen = false;
     tile_best<EB, false>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid, packed,
                          bits, nan_seen, after_first_loads);
-    __shared__ int s_nan[kWaves];
+    // Every thread learns the tile's best pair and whether any wavefront saw a
+    // NaN, so every thread takes the same decision without a second barrier.
     const bool wave_nan = __ballot(nan_seen) != 0ull;
-    if ((tid & 63) == 0) s_nan[tid >> 6] = wave_nan;
-    block_reduce(packed, bits);          // its barrier also publishes s_nan
-    __shared__ int s_again;
-    if (tid == 0) {
-        int any_nan = packed_key(packed) > KeyTraits<EB>::kInf;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) any_nan |= s_nan[w];
-        s_again = any_nan;
-    }
-    __syncthreads();
-    if (s_again) {
+    const bool any_nan = block_reduce(packed, bits, wave_nan);
+    if (any_nan || packed_key(packed) > KeyTraits<EB>::kInf) {
+        __syncthreads();                 // every thread has read the first reduction
         tile_best<EB, true>(row_ptr, geom, vocab, col_offset, split, splits, chunk_vecs, tid,
                             packed, bits, nan_seen, [] {});
-        block_reduce(packed, bits);
+        block_reduce(packed, bits, false);
     }
     if (tid != 0) return;
     const uint32_t draft_bits = owns_x ? (EB == 2 ? draft_raw << 16 : draft_raw) : 0u;
