@@ -268,6 +268,18 @@ __device__ __forceinline__ void dpp_max_step(unsigned long long& p, uint32_t& bi
     bits = take ? qb : bits;
 }
 
+// Unsigned 64-bit maximum of a lane's value and that of the lane `kCtrl`
+// names (a DPP pattern in which every lane has a source).
+template <int kCtrl>
+__device__ __forceinline__ unsigned long long dpp_umax64(unsigned long long p) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)p, kCtrl, 0xf, 0xf,
+                                                              false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(p >> 32), kCtrl,
+                                                              0xf, 0xf, false);
+    const unsigned long long q = ((unsigned long long)hi << 32) | lo;
+    return q > p ? q : p;
+}
+
 // Workgroup-wide maximum of (packed, bits), and the OR of one flag per
 // wavefront; every thread returns with both.  Within a wavefront, shifts of 1,
 // 2, 4 and 8 lanes make lane 15 of each 16-lane row hold the row's maximum,
@@ -1520,12 +1532,12 @@ __global__ __launch_bounds__(kLmThreads) void asd_lmhead_kernel(
                 row_draft_bits[row0 + r] = fv[(int)xo & 3];
             }
         }
-        unsigned long long o = __shfl_xor(best, 1, 64);
-        best = o > best ? o : best;
-        o = __shfl_xor(best, 2, 64);
-        best = o > best ? o : best;
-        o = __shfl_xor(best, 4, 64);
-        best = o > best ? o : best;
+        // The eight threads of a row (lanes 8k .. 8k + 7) combine by DPP: the
+        // lane pairs and quad pairs of quad_perm, then the mirror within each
+        // eight-lane half row.
+        best = dpp_umax64<0xb1>(best);                     // quad_perm [1, 0, 3, 2]
+        best = dpp_umax64<0x4e>(best);                     // quad_perm [2, 3, 0, 1]
+        best = dpp_umax64<0x141>(best);                    // row_half_mirror
         if (q == 0 && row0 + r < M) atomicMax(row_best + row0 + r, best);
     }
 }
